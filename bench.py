@@ -1,0 +1,190 @@
+#!/usr/bin/env python3
+"""Throughput of one Fast-dLLM++ decoding step on one MI355X.
+
+Workload (throughput stress recipe): B=1024 sequences, an active block of
+L=32 all-masked positions each, V=126464 bf16 logits per position (8.29 GB
+per step, Gumbel(0,1) background with 10% planted near-ties), resident in HBM.
+A step is the whole hot path in one fused launch: the vocabulary pass
+(greedy token, confidence, eps, lse for all 32768 positions), the Frechet
+profile selection (f = 1.0) of every block and the reveal.  Each timed step
+first restores the step's input mask/x (two small device copies), so every
+step does the same work.
+
+Prints one JSON line.  `value` is masked positions per second over the whole
+timed region; `roofline` relates the fused kernel's algorithmic bytes to its
+average launch time measured with HIP events on the launch stream.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "masked positions selected/sec + logits-read HBM GB/s (% of peak), 1 GPU"
+HBM_PEAK_GBPS = 8000.0
+IO_BYTES_PER_POSITION = 18   # mask read, commit, tokens, conf, eps, lse (1+1+4+4+4+4)
+SRC = os.path.join(ROOT, "paper_2606_02955_amd", "csrc", "fdllm.hip")
+TRAFFIC = os.path.join(ROOT, "profiles", "traffic_fused_decode_config5.json")
+
+
+def source_digest() -> str:
+    return hashlib.sha256(open(SRC, "rb").read()).hexdigest()[:16]
+
+
+def measured_traffic():
+    """HBM bytes per launch from committed rocprofv3 counter runs, if current."""
+    try:
+        t = json.load(open(TRAFFIC))
+    except (OSError, ValueError):
+        return None
+    if t.get("source_sha256_16") != source_digest():
+        return None
+    return t.get("hbm_bytes_per_launch")
+
+
+def cpu_baseline(inp, n_blocks: int, rule: str, param: float):
+    """The oracle on a bounded, seeded sample of blocks of the same step."""
+    import numpy as np
+    import oracle
+    B, L, V = inp.logits.shape
+    rng = np.random.default_rng(7)
+    blocks = sorted(rng.choice(B, n_blocks, replace=False).tolist())
+    rows = inp.logits[blocks].to("cpu")                      # [n, L, V] bf16, outside the timing
+    mask = inp.mask[blocks].cpu().numpy()
+    start, end = inp.start[blocks].cpu().numpy(), inp.end[blocks].cpu().numpy()
+    x = inp.x[blocks].cpu().numpy()
+    get = lambda b, i: rows[b, i].to(dtype=__import__("torch").float64).numpy()
+    t0 = time.perf_counter()
+    r = oracle.decode_step(get, n_blocks, L, mask, start, end, x, rule, param)
+    dt = time.perf_counter() - t0
+    n_pos = int(mask.sum())
+    return {"value": n_pos / dt, "unit": "masked positions/s", "cores": 1, "kind": "oracle",
+            "sample": f"{n_blocks} of {B} blocks ({n_pos} positions, {n_pos * V * 2 / 1e9:.2f} GB of "
+                      f"bf16 logits) of the same step, {rule} f={param}; single-threaded NumPy "
+                      f"float64 + exact rational selection; {dt:.1f} s",
+            "seconds": dt, "host_cpus_available": len(os.sched_getaffinity(0)),
+            "commits": int(r.n_commit.sum())}
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--selector", default="profile", choices=["profile", "factor", "threshold"])
+    ap.add_argument("--param", type=float, default=None, help="f (default 1.0) or tau (default 0.9)")
+    ap.add_argument("--cpu-blocks", type=int, default=40, help="blocks in the oracle sample")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-selector-sweep", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only; --gpus {args.gpus} is not supported "
+              f"(sequences shard across GPUs with no exchange, so the per-GPU figure is the one-GPU run)",
+              file=sys.stderr)
+        sys.exit(2)
+    param = args.param if args.param is not None else (0.9 if args.selector == "threshold" else 1.0)
+
+    import torch
+    import paper_2606_02955_amd as fd
+    import workloads
+
+    fd.load()
+    dev = torch.device("cuda", 0)
+    torch.cuda.set_device(dev)
+    print(f"[bench] generating config5 inputs on {torch.cuda.get_device_name(dev)}", file=sys.stderr, flush=True)
+    inp = workloads.config5(device=dev)
+    B, L, V = inp.logits.shape
+    positions = int(inp.mask.sum())
+    logits_bytes = positions * V * inp.logits.element_size()
+    algo_bytes = logits_bytes + B * L * IO_BYTES_PER_POSITION + B * 12
+    mask0, x0 = inp.mask.clone(), inp.x.clone()
+    mask, x = inp.mask.clone(), inp.x.clone()
+    outs = dict(tokens=torch.empty((B, L), dtype=torch.int32, device=dev),
+                conf=torch.empty((B, L), device=dev), eps=torch.empty((B, L), device=dev),
+                lse=torch.empty((B, L), device=dev),
+                commit=torch.empty((B, L), dtype=torch.uint8, device=dev),
+                n_commit=torch.empty((B,), dtype=torch.int32, device=dev))
+    torch.cuda.synchronize()
+
+    def run(selector, p, steps, warmup, label):
+        evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+               for _ in range(steps)]
+        for _ in range(warmup):
+            mask.copy_(mask0); x.copy_(x0)
+            fd.fdllm_decode_step(inp.logits, mask, inp.start, inp.end, x, selector, p, **outs)
+        torch.cuda.synchronize()
+        print(f"[bench] {label}: timing {steps} steps", file=sys.stderr, flush=True)
+        t0 = time.perf_counter()
+        for k in range(steps):
+            mask.copy_(mask0); x.copy_(x0)
+            evs[k][0].record()
+            fd.fdllm_decode_step(inp.logits, mask, inp.start, inp.end, x, selector, p, **outs)
+            evs[k][1].record()
+        torch.cuda.synchronize()
+        wall = time.perf_counter() - t0
+        kern = [a.elapsed_time(b) * 1e-3 for a, b in evs]
+        return wall, sum(kern) / len(kern), min(kern)
+
+    wall, kavg, kmin = run(args.selector, param, args.steps, args.warmup, f"{args.selector}({param})")
+    commits = float(outs["n_commit"].float().mean())
+    sweep = {}
+    if not args.no_selector_sweep:
+        for sel, p in [("profile", 1.0), ("profile", 0.75), ("factor", 1.0), ("factor", 0.75),
+                       ("threshold", 0.9)]:
+            if sel == args.selector and p == param:
+                continue
+            w2, k2, _ = run(sel, p, max(5, args.steps // 4), 1, f"{sel}({p})")
+            sweep[f"{sel}({p})"] = {"ms_per_step": 1e3 * w2 / max(5, args.steps // 4),
+                                    "kernel_ms": 1e3 * k2,
+                                    "mean_commits_per_block": float(outs["n_commit"].float().mean())}
+    ms = 1e3 * wall / args.steps
+    value = positions * args.steps / wall
+    achieved = algo_bytes / kavg / 1e9
+    traffic = measured_traffic()
+    line = {
+        "metric": METRIC,
+        "value": value,
+        "unit": "masked positions/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {"workload": "config5 throughput stress: B=1024 blocks x L=32 masked positions, "
+                               "V=126464 bf16 logits (Gumbel(0,1), 10% planted near-ties), one fused "
+                               f"decode step ({args.selector} {'tau' if args.selector == 'threshold' else 'f'}={param})",
+                   "B": B, "L": L, "V": V, "logits_dtype": "bf16", "selector": args.selector,
+                   "param": param, "parallelism": "none (1 GPU)"},
+        "logits_read_GBps": logits_bytes * args.steps / wall / 1e9,
+        "logits_read_frac_of_peak": logits_bytes * args.steps / wall / 1e9 / HBM_PEAK_GBPS,
+        "kernel_ms_avg": 1e3 * kavg,
+        "kernel_ms_min": 1e3 * kmin,
+        "mean_commits_per_block": commits,
+        "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBPS, "unit": "GB/s",
+                     "frac": achieved / HBM_PEAK_GBPS,
+                     "traffic": traffic,
+                     "kernel": "k_fused (one launch per step)",
+                     "algorithmic_bytes_per_launch": algo_bytes},
+        "selectors": sweep,
+        "source_sha256_16": source_digest(),
+    }
+    if not args.no_cpu_baseline:
+        print(f"[bench] cpu_baseline: oracle on {args.cpu_blocks} blocks", file=sys.stderr, flush=True)
+        line["cpu_baseline"] = cpu_baseline(inp, args.cpu_blocks, args.selector, param)
+    else:
+        line["cpu_baseline"] = None
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

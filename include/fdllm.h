@@ -1,0 +1,178 @@
+/*
+ * fdllm.h -- C ABI of the Fast-dLLM++ commit selector for AMD Instinct MI355X
+ * (gfx950).  Implements one decoding step of Frechet profile decoding
+ * (arXiv 2606.02955, Alg. 1): per masked position of the active block the
+ * greedy token and its softmax confidence, per block the commit set chosen by
+ * the Frechet profile rule (or the factor / threshold baselines), and the
+ * reveal of the chosen tokens.
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ * Pointers.  Every array pointer is DEVICE memory owned by the caller
+ *   (allocated with hipMalloc or by a framework such as PyTorch).  The library
+ *   never allocates, frees or retains a pointer beyond the call.
+ * Layout.  Arrays are contiguous and row-major:
+ *   logits [B, L, V]            bf16 (FDLLM_BF16) or fp32 (FDLLM_F32)
+ *   mask   [B, L]  uint8        1 = position still masked
+ *   x      [B, L]  int32        sequence tokens
+ *   tokens [B, L]  int32        greedy token (argmax over V)
+ *   conf   [B, L]  float        confidence c = max_v softmax(logits)_v
+ *   eps    [B, L]  float        1 - c, computed without cancellation
+ *   lse    [B, L]  float        log sum_v exp(logits_v)
+ *   commit [B, L]  uint8        1 = position revealed this step
+ *   n_commit [B]   int32        number of revealed positions per sequence
+ *   block_start, block_end [B] int32: sequence b's active block is the
+ *   half-open span [block_start[b], block_end[b]) of its L positions.
+ *   The L rows may be the active block itself (start 0, end L: logits of a
+ *   cached model call) or a longer span of which the bounds select the block.
+ * Candidates.  Position i of sequence b is a candidate when
+ *   block_start[b] <= i < block_end[b] and mask[b, i] != 0 (Alg. 1 visits the
+ *   masked positions of the active block).  Logits of other rows are never
+ *   read; their outputs are tokens = -1, conf = 0, eps = 1, lse = 0,
+ *   commit = 0.
+ * Bounds.  A block needs 0 <= start <= end <= L and end - start <= 64
+ *   (FDLLM_MAX_BLOCK, one 64-lane wavefront).  Bounds live in device memory
+ *   and are checked on the device: a sequence with invalid bounds gets no
+ *   commits, default outputs and n_commit = -1.
+ * Logits.  Must be finite with |logit| < 1e30 (NaN/inf are not supported).
+ * Ties.  The argmax takes the lowest vocabulary index; the confidence sort
+ *   puts equal values at the lower position first.
+ * Streams.  Every call only enqueues work on `stream` (NULL = the null
+ *   stream) and returns; results are visible after stream synchronisation.
+ *   Kernel faults surface at that synchronisation.
+ * Errors.  Argument checks are done on the host before anything is enqueued;
+ *   a failing check returns a negative status and enqueues nothing.
+ * Determinism.  For fixed (B, L, V, dtype) every call is bitwise
+ *   reproducible, identical rows give bitwise identical outputs, and
+ *   fdllm_decode_step gives bitwise the same tokens/conf/eps/lse as
+ *   fdllm_confidence and the same commits as fdllm_select_* fed with them.
+ */
+#ifndef FDLLM_H
+#define FDLLM_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* A hipStream_t (same underlying type); NULL selects the null stream. */
+typedef struct ihipStream_t* fdllm_stream;
+
+typedef enum { FDLLM_BF16 = 0, FDLLM_F32 = 1 } fdllm_dtype;
+
+typedef enum {
+  FDLLM_SEL_THRESHOLD = 0, /* commit every c >= tau, else the single highest      */
+  FDLLM_SEL_FACTOR = 1,    /* largest n with (n+1)(1 - c_(n)) < f                 */
+  FDLLM_SEL_PROFILE = 2    /* largest n with G_n > 1 - f (Frechet profile rule)   */
+} fdllm_selector;
+
+typedef int fdllm_status;
+#define FDLLM_OK 0
+#define FDLLM_ERR_INVALID_ARG (-1)       /* null pointer, negative size, bad enum   */
+#define FDLLM_ERR_UNSUPPORTED_DTYPE (-2) /* dtype not FDLLM_BF16 / FDLLM_F32         */
+#define FDLLM_ERR_SIZE (-3)              /* V < 1, or B*L*V beyond 2^62 elements     */
+#define FDLLM_ERR_WORKSPACE (-4)         /* workspace missing or too small           */
+#define FDLLM_ERR_HIP (-5)               /* the HIP runtime rejected a launch        */
+
+#define FDLLM_MAX_BLOCK 64
+
+/*
+ * Greedy token, confidence, complement and log-sum-exp of every candidate
+ * position (Sec. 3 "Notation": x*_i = argmax_v p_i(v), c_i = p_i(x*_i); Alg. 1
+ * per-position loop; softmax at temperature 1 as in greedy decoding).  Each
+ * logit of a candidate row is read exactly once.
+ *   logits  [B,L,V] bf16/fp32 per `dtype`        (in)
+ *   mask    [B,L] uint8                           (in)
+ *   block_start, block_end [B] int32              (in)
+ *   tokens  [B,L] int32                           (out, required)
+ *   conf    [B,L] float                           (out, required)
+ *   eps     [B,L] float                           (out, may be NULL)
+ *   lse     [B,L] float                           (out, may be NULL)
+ */
+fdllm_status fdllm_confidence(const void* logits, fdllm_dtype dtype, int B, int L, int V,
+                              const uint8_t* mask, const int32_t* block_start,
+                              const int32_t* block_end, int32_t* tokens, float* conf, float* eps,
+                              float* lse, fdllm_stream stream);
+
+/*
+ * Commit set of each block from per-position confidences (phase after the
+ * vocabulary pass).  Candidates are ordered by confidence descending --
+ * by eps ascending when `eps` is given, else by conf descending -- with
+ * ties to the lower position; this is the sort of Alg. 1.
+ *
+ * fdllm_select_profile: Frechet profile rule (Sec. 3 "Frechet profile
+ *   quantities"; Alg. 1 selection).  With c_(j) the sorted confidences,
+ *   L_n = max{0, sum_{j<=n} c_(j) - (n-1)}, U_n = 1 - c_(n), G_n = L_n - U_n,
+ *   n* = max{n : G_n > delta}, delta = 1 - f (matched parameterisation,
+ *   equal-confidence corollary and Sec. 5), n* = 1 when no n qualifies.  It
+ *   is evaluated as (n+1)(1 - c_(n)) - B_n < f with the heterogeneity bonus
+ *   B_n = sum_{j<n} (c_(j) - c_(n)) (adaptive-factor remark), which accepts
+ *   exactly the same n as the clipped definition for f <= 1 and is the rule
+ *   used for f > 1.
+ * fdllm_select_factor: Fast-dLLM factor rule (Sec. 2; Sec. 5 "Baselines"):
+ *   largest n with (n+1)(1 - c_(n)) < f, else 1.
+ * fdllm_select_threshold: (Sec. 2) every candidate with conf >= tau; when
+ *   none qualifies, the single highest-confidence candidate.
+ * Arguments:
+ *   conf [B,L] float (in, required); eps [B,L] float (in, may be NULL: then
+ *   eps = 1 - conf exactly); mask, block_start, block_end as above (in);
+ *   param: f for profile/factor, tau for threshold;
+ *   commit [B,L] uint8 (out, required; every entry written);
+ *   n_commit [B] int32 (out, may be NULL).
+ * The criterion is evaluated in double precision on the given float values.
+ */
+fdllm_status fdllm_select_profile(const float* conf, const float* eps, const uint8_t* mask,
+                                  const int32_t* block_start, const int32_t* block_end, int B,
+                                  int L, float f, uint8_t* commit, int32_t* n_commit,
+                                  fdllm_stream stream);
+fdllm_status fdllm_select_factor(const float* conf, const float* eps, const uint8_t* mask,
+                                 const int32_t* block_start, const int32_t* block_end, int B,
+                                 int L, float f, uint8_t* commit, int32_t* n_commit,
+                                 fdllm_stream stream);
+fdllm_status fdllm_select_threshold(const float* conf, const float* eps, const uint8_t* mask,
+                                    const int32_t* block_start, const int32_t* block_end, int B,
+                                    int L, float tau, uint8_t* commit, int32_t* n_commit,
+                                    fdllm_stream stream);
+
+/*
+ * Reveal (Alg. 1, reveal step): for every (b,i) with commit[b,i] != 0 set
+ * x[b,i] = tokens[b,i] and mask[b,i] = 0.  Other entries are untouched.
+ *   commit [B,L] uint8 (in); tokens [B,L] int32 (in); x [B,L] int32 (in/out);
+ *   mask [B,L] uint8 (in/out).
+ */
+fdllm_status fdllm_reveal(const uint8_t* commit, const int32_t* tokens, int32_t* x, uint8_t* mask,
+                          int B, int L, fdllm_stream stream);
+
+/*
+ * One whole decoding step (Alg. 1, loop body after the model call):
+ * fdllm_confidence, then the selector `sel` with `param` (f, or tau for the
+ * threshold rule), then the reveal, fused.  Large batches run as one kernel
+ * (one workgroup per sequence); small batches as two kernels.
+ *   mask [B,L] uint8 (in/out: committed positions are cleared);
+ *   x    [B,L] int32 (in/out: committed positions receive their token);
+ *   tokens, conf, eps, lse [B,L], commit [B,L], n_commit [B]: optional
+ *   outputs (NULL to skip), with the meanings above.
+ *   workspace: device memory of at least fdllm_workspace_size() bytes
+ *   (may be NULL when that size is 0); its contents need no initialisation
+ *   and are scratch between calls.
+ */
+fdllm_status fdllm_decode_step(const void* logits, fdllm_dtype dtype, int B, int L, int V,
+                               uint8_t* mask, const int32_t* block_start, const int32_t* block_end,
+                               int32_t* x, fdllm_selector sel, float param, int32_t* tokens,
+                               float* conf, float* eps, float* lse, uint8_t* commit,
+                               int32_t* n_commit, void* workspace, size_t workspace_bytes,
+                               fdllm_stream stream);
+
+/* Workspace bytes fdllm_decode_step needs for these sizes (0 = none). */
+fdllm_status fdllm_workspace_size(int B, int L, int V, fdllm_dtype dtype, size_t* bytes);
+
+/* Static, human-readable text for a status code. */
+const char* fdllm_status_string(fdllm_status status);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* FDLLM_H */

@@ -1,0 +1,187 @@
+"""Python binding of libfdllm.so, the gfx950 Fast-dLLM++ commit selector.
+
+Thin ctypes marshalling of the C ABI declared in include/fdllm.h: every
+function takes torch tensors that already live on the GPU, checks their
+dtype/shape/contiguity, and passes raw device pointers plus the current HIP
+stream.  All arithmetic happens in the HIP kernels; there is no CPU fallback,
+and loading fails loudly when the library has not been built.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional
+
+import torch
+
+_PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_PKG, "libfdllm.so")
+
+BF16, F32 = 0, 1
+SEL_THRESHOLD, SEL_FACTOR, SEL_PROFILE = 0, 1, 2
+SELECTORS = {"threshold": SEL_THRESHOLD, "factor": SEL_FACTOR, "profile": SEL_PROFILE}
+MAX_BLOCK = 64
+
+OK = 0
+ERR_INVALID_ARG, ERR_UNSUPPORTED_DTYPE, ERR_SIZE, ERR_WORKSPACE, ERR_HIP = -1, -2, -3, -4, -5
+
+EXPORTS = ("fdllm_confidence", "fdllm_select_profile", "fdllm_select_factor",
+           "fdllm_select_threshold", "fdllm_reveal", "fdllm_decode_step",
+           "fdllm_workspace_size", "fdllm_status_string")
+
+_lib = None
+
+
+class FdllmError(RuntimeError):
+    def __init__(self, status: int, where: str):
+        self.status = status
+        super().__init__(f"{where}: {status_string(status)} (status {status})")
+
+
+def load(path: Optional[str] = None) -> ctypes.CDLL:
+    """Load libfdllm.so (built by paper_2606_02955_amd.build); raises if absent."""
+    global _lib
+    if _lib is not None and path is None:
+        return _lib
+    p = path or LIB_PATH
+    if not os.path.exists(p):
+        raise FileNotFoundError(
+            f"{p} is missing: build it first (python -m paper_2606_02955_amd.build)")
+    lib = ctypes.CDLL(p)
+    vp, i32, f32, sz = ctypes.c_void_p, ctypes.c_int, ctypes.c_float, ctypes.c_size_t
+    lib.fdllm_confidence.argtypes = [vp, i32, i32, i32, i32, vp, vp, vp, vp, vp, vp, vp, vp]
+    for name in ("fdllm_select_profile", "fdllm_select_factor", "fdllm_select_threshold"):
+        getattr(lib, name).argtypes = [vp, vp, vp, vp, vp, i32, i32, f32, vp, vp, vp]
+        getattr(lib, name).restype = i32
+    lib.fdllm_reveal.argtypes = [vp, vp, vp, vp, i32, i32, vp]
+    lib.fdllm_decode_step.argtypes = [vp, i32, i32, i32, i32, vp, vp, vp, vp, i32, f32,
+                                      vp, vp, vp, vp, vp, vp, vp, sz, vp]
+    lib.fdllm_workspace_size.argtypes = [i32, i32, i32, i32, ctypes.POINTER(sz)]
+    lib.fdllm_status_string.argtypes = [i32]
+    lib.fdllm_status_string.restype = ctypes.c_char_p
+    for name in ("fdllm_confidence", "fdllm_reveal", "fdllm_decode_step", "fdllm_workspace_size"):
+        getattr(lib, name).restype = i32
+    if path is None:
+        _lib = lib
+    return lib
+
+
+def status_string(status: int) -> str:
+    return load().fdllm_status_string(int(status)).decode()
+
+
+def _check(status: int, where: str):
+    if status != OK:
+        raise FdllmError(status, where)
+
+
+def _ptr(t: Optional[torch.Tensor], dtype=None, shape=None, name="tensor"):
+    if t is None:
+        return None
+    if not t.is_cuda:
+        raise ValueError(f"{name} must be a GPU tensor")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    if dtype is not None and t.dtype != dtype:
+        raise ValueError(f"{name} must be {dtype}, got {t.dtype}")
+    if shape is not None and tuple(t.shape) != tuple(shape):
+        raise ValueError(f"{name} must have shape {tuple(shape)}, got {tuple(t.shape)}")
+    return ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(device) -> ctypes.c_void_p:
+    return ctypes.c_void_p(torch.cuda.current_stream(device).cuda_stream)
+
+
+def _dtype_code(t: torch.Tensor) -> int:
+    if t.dtype == torch.bfloat16:
+        return BF16
+    if t.dtype == torch.float32:
+        return F32
+    raise ValueError(f"logits must be bfloat16 or float32, got {t.dtype}")
+
+
+def fdllm_confidence(logits, mask, block_start, block_end, tokens, conf, eps=None, lse=None):
+    """Greedy token / confidence / eps / lse of every candidate (see fdllm.h)."""
+    B, L, V = logits.shape
+    lib = load()
+    st = lib.fdllm_confidence(
+        _ptr(logits, name="logits"), _dtype_code(logits), B, L, V,
+        _ptr(mask, torch.uint8, (B, L), "mask"), _ptr(block_start, torch.int32, (B,), "block_start"),
+        _ptr(block_end, torch.int32, (B,), "block_end"), _ptr(tokens, torch.int32, (B, L), "tokens"),
+        _ptr(conf, torch.float32, (B, L), "conf"), _ptr(eps, torch.float32, (B, L), "eps"),
+        _ptr(lse, torch.float32, (B, L), "lse"), _stream(logits.device))
+    _check(st, "fdllm_confidence")
+
+
+def _select(name, conf, eps, mask, block_start, block_end, param, commit, n_commit=None):
+    B, L = conf.shape
+    lib = load()
+    st = getattr(lib, name)(
+        _ptr(conf, torch.float32, (B, L), "conf"), _ptr(eps, torch.float32, (B, L), "eps"),
+        _ptr(mask, torch.uint8, (B, L), "mask"), _ptr(block_start, torch.int32, (B,), "block_start"),
+        _ptr(block_end, torch.int32, (B,), "block_end"), B, L, float(param),
+        _ptr(commit, torch.uint8, (B, L), "commit"), _ptr(n_commit, torch.int32, (B,), "n_commit"),
+        _stream(conf.device))
+    _check(st, name)
+
+
+def fdllm_select_profile(conf, eps, mask, block_start, block_end, f, commit, n_commit=None):
+    _select("fdllm_select_profile", conf, eps, mask, block_start, block_end, f, commit, n_commit)
+
+
+def fdllm_select_factor(conf, eps, mask, block_start, block_end, f, commit, n_commit=None):
+    _select("fdllm_select_factor", conf, eps, mask, block_start, block_end, f, commit, n_commit)
+
+
+def fdllm_select_threshold(conf, eps, mask, block_start, block_end, tau, commit, n_commit=None):
+    _select("fdllm_select_threshold", conf, eps, mask, block_start, block_end, tau, commit, n_commit)
+
+
+def fdllm_reveal(commit, tokens, x, mask):
+    B, L = commit.shape
+    st = load().fdllm_reveal(
+        _ptr(commit, torch.uint8, (B, L), "commit"), _ptr(tokens, torch.int32, (B, L), "tokens"),
+        _ptr(x, torch.int32, (B, L), "x"), _ptr(mask, torch.uint8, (B, L), "mask"), B, L,
+        _stream(commit.device))
+    _check(st, "fdllm_reveal")
+
+
+def fdllm_workspace_size(B: int, L: int, V: int, dtype: torch.dtype) -> int:
+    n = ctypes.c_size_t(0)
+    code = BF16 if dtype == torch.bfloat16 else F32 if dtype == torch.float32 else -1
+    _check(load().fdllm_workspace_size(B, L, V, code, ctypes.byref(n)), "fdllm_workspace_size")
+    return int(n.value)
+
+
+def fdllm_decode_step(logits, mask, block_start, block_end, x, selector: str, param: float,
+                      tokens=None, conf=None, eps=None, lse=None, commit=None, n_commit=None,
+                      workspace: Optional[torch.Tensor] = None):
+    """One fused decoding step; mask and x are updated in place (see fdllm.h)."""
+    B, L, V = logits.shape
+    if selector not in SELECTORS:
+        raise ValueError(f"selector must be one of {sorted(SELECTORS)}")
+    need = fdllm_workspace_size(B, L, V, logits.dtype)
+    ws_ptr, ws_bytes = None, 0
+    if workspace is not None:
+        ws_ptr, ws_bytes = _ptr(workspace, name="workspace"), workspace.numel() * workspace.element_size()
+    elif need and (tokens is None or conf is None or eps is None):
+        workspace = torch.empty(need, dtype=torch.uint8, device=logits.device)
+        ws_ptr, ws_bytes = _ptr(workspace), need
+    st = load().fdllm_decode_step(
+        _ptr(logits, name="logits"), _dtype_code(logits), B, L, V,
+        _ptr(mask, torch.uint8, (B, L), "mask"), _ptr(block_start, torch.int32, (B,), "block_start"),
+        _ptr(block_end, torch.int32, (B,), "block_end"), _ptr(x, torch.int32, (B, L), "x"),
+        SELECTORS[selector], float(param),
+        _ptr(tokens, torch.int32, (B, L), "tokens"), _ptr(conf, torch.float32, (B, L), "conf"),
+        _ptr(eps, torch.float32, (B, L), "eps"), _ptr(lse, torch.float32, (B, L), "lse"),
+        _ptr(commit, torch.uint8, (B, L), "commit"), _ptr(n_commit, torch.int32, (B,), "n_commit"),
+        ws_ptr, ws_bytes, _stream(logits.device))
+    _check(st, "fdllm_decode_step")
+    return workspace
+
+
+def select(selector: str, conf, eps, mask, block_start, block_end, param, commit, n_commit=None):
+    {"profile": fdllm_select_profile, "factor": fdllm_select_factor,
+     "threshold": fdllm_select_threshold}[selector](conf, eps, mask, block_start, block_end,
+                                                    param, commit, n_commit)

@@ -1,0 +1,929 @@
+// fdllm.hip -- gfx950 kernels and C ABI of the Fast-dLLM++ commit selector.
+//
+// One decoding step of Frechet profile decoding (arXiv 2606.02955, Alg. 1):
+//   (1) vocabulary pass: per candidate position, the greedy token, its softmax
+//       confidence c, the complement eps = 1 - c and the log-sum-exp
+//       (Sec. 3 "Notation"); every logit of a candidate row is read once;
+//   (2) selection: per block, sort the <= 64 candidates by confidence and
+//       apply the Frechet profile / factor / threshold rule (Sec. 3
+//       "Frechet profile quantities", Sec. 2, Sec. 5 "Baselines");
+//   (3) reveal: write the chosen tokens into the sequence and clear their mask.
+//
+// The vocabulary pass is bound by HBM bandwidth: per logit it does one
+// exp2, a few VALU ops and no reuse, so there is no dense contraction and
+// no MFMA.  Design:
+//   * a row is streamed by one wavefront (or split over S wavefronts for
+//     small batches) with 16-byte loads; lane l of the wave reads vectors
+//     l, l+64, ... so every wave-wide load is 1 KiB contiguous;
+//   * loads are grouped in batches of U vectors per lane; for each batch the
+//     lane first takes the batch maximum (v_max3), then adds
+//     2^(x*log2e - K) for every element into a double accumulator.  K is an
+//     integer-valued float, K = ceil(m * log2e) for the running maximum m,
+//     so rescaling the accumulator when m grows is an exact ldexp.  The
+//     greedy element enters the sum as exactly the value the final step
+//     recomputes, so s' = sum_{v != t} exp(l_v - M) is recovered by an
+//     exact subtraction and eps keeps its relative accuracy when c -> 1;
+//   * the argmax is tracked per batch (the batch in which the lane's maximum
+//     first appeared); at the end, lanes holding the row maximum re-read
+//     that batch to find the lowest index, then a wave minimum gives the
+//     lowest index of the whole row;
+//   * wavefront reductions use DPP row operations, ds_swizzle and
+//     v_readlane; partials of a split row meet in LDS in fixed order, so
+//     results do not depend on scheduling.
+// The selection runs in one wavefront per block: a 64-lane bitonic sort of
+// (eps bits, slot) keys, a double-precision prefix scan of the heterogeneity
+// bonus, a ballot for n*, and ds_permute to route each decision back to its
+// position.
+#include <hip/hip_runtime.h>
+
+#include <math.h>
+#include <stdint.h>
+
+#include "fdllm.h"
+
+namespace fdllm {
+
+constexpr int kWave = 64;
+constexpr int kMaxBlock = FDLLM_MAX_BLOCK;
+constexpr float kLog2e = 1.44269504088896340736f;
+constexpr float kNegInf = -__builtin_huge_valf();
+constexpr float kRefFloor = -3.0e38f;   // exponent reference before any element
+
+// ---------------------------------------------------------------------------
+// wavefront primitives (wave64)
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ int lane_id() { return __builtin_amdgcn_mbcnt_hi(~0u, __builtin_amdgcn_mbcnt_lo(~0u, 0u)); }
+
+// DPP controls (gfx9): quad_perm, row_half_mirror, row_mirror.
+constexpr int kDppXor1 = 0xB1;        // quad_perm [1,0,3,2]
+constexpr int kDppXor2 = 0x4E;        // quad_perm [2,3,0,1]
+constexpr int kDppHalfMirror = 0x141; // lane i <-> 7-i within 8 (xor 4 once quads agree)
+constexpr int kDppMirror = 0x140;     // lane i <-> 15-i within 16 (xor 8 once octets agree)
+constexpr int kSwzXor16 = 0x401F;     // ds_swizzle bit mode: and 0x1F, xor 0x10
+
+template <int Ctrl>
+__device__ __forceinline__ int dpp(int v) {
+  return __builtin_amdgcn_update_dpp(0, v, Ctrl, 0xF, 0xF, false);
+}
+
+// Butterfly all-reduce step helpers: return the partner's value for step s.
+// Steps 0..3 are DPP, step 4 is ds_swizzle (within 32 lanes); the final
+// 32-lane exchange is done with readlane by the callers.
+template <int Step>
+__device__ __forceinline__ int partner_i32(int v) {
+  if constexpr (Step == 0) return dpp<kDppXor1>(v);
+  else if constexpr (Step == 1) return dpp<kDppXor2>(v);
+  else if constexpr (Step == 2) return dpp<kDppHalfMirror>(v);
+  else if constexpr (Step == 3) return dpp<kDppMirror>(v);
+  else return __builtin_amdgcn_ds_swizzle(v, kSwzXor16);
+}
+
+template <int Step>
+__device__ __forceinline__ float partner_f32(float v) {
+  return __int_as_float(partner_i32<Step>(__float_as_int(v)));
+}
+
+template <int Step>
+__device__ __forceinline__ double partner_f64(double v) {
+  long long b = __double_as_longlong(v);
+  int lo = partner_i32<Step>((int)(b & 0xffffffffll));
+  int hi = partner_i32<Step>((int)(b >> 32));
+  return __longlong_as_double(((long long)hi << 32) | (unsigned int)lo);
+}
+
+__device__ __forceinline__ float readlane_f32(float v, int l) {
+  return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), l));
+}
+__device__ __forceinline__ double readlane_f64(double v, int l) {
+  long long b = __double_as_longlong(v);
+  int lo = __builtin_amdgcn_readlane((int)(b & 0xffffffffll), l);
+  int hi = __builtin_amdgcn_readlane((int)(b >> 32), l);
+  return __longlong_as_double(((long long)hi << 32) | (unsigned int)lo);
+}
+
+__device__ __forceinline__ float wave_max(float v) {
+  v = fmaxf(v, partner_f32<0>(v));
+  v = fmaxf(v, partner_f32<1>(v));
+  v = fmaxf(v, partner_f32<2>(v));
+  v = fmaxf(v, partner_f32<3>(v));
+  v = fmaxf(v, partner_f32<4>(v));
+  return fmaxf(readlane_f32(v, 0), readlane_f32(v, 32));
+}
+
+__device__ __forceinline__ int wave_min(int v) {
+  v = min(v, partner_i32<0>(v));
+  v = min(v, partner_i32<1>(v));
+  v = min(v, partner_i32<2>(v));
+  v = min(v, partner_i32<3>(v));
+  v = min(v, partner_i32<4>(v));
+  return min(__builtin_amdgcn_readlane(v, 0), __builtin_amdgcn_readlane(v, 32));
+}
+
+// ---------------------------------------------------------------------------
+// exponent reference and per-element term.  Shared by the streaming loop
+// and the final step, so the greedy element's term is recomputed bit-exactly.
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ float exp_ref(float m) { return ceilf(m * kLog2e); }
+__device__ __forceinline__ float term(float x, float K) {
+  return __builtin_amdgcn_exp2f(__builtin_fmaf(x, kLog2e, -K));
+}
+// 2^(a - b) applied to s, with a <= b integer-valued floats (exact).
+__device__ __forceinline__ double rescale(double s, float a, float b) {
+  float d = fmaxf(a - b, -2000.0f);
+  return ldexp(s, (int)d);
+}
+
+// (K, S) pair combine: both sums brought to the larger reference.
+__device__ __forceinline__ void ks_combine(float& K, double& S, float K2, double S2) {
+  float Kn = fmaxf(K, K2);
+  S = rescale(S, K, Kn) + rescale(S2, K2, Kn);
+  K = Kn;
+}
+
+template <int Step>
+__device__ __forceinline__ void ks_step(float& K, double& S) {
+  float K2 = partner_f32<Step>(K);
+  double S2 = partner_f64<Step>(S);
+  ks_combine(K, S, K2, S2);
+}
+
+// ---------------------------------------------------------------------------
+// vector formats: one lane loads 16 bytes (or one element on the scalar path)
+// ---------------------------------------------------------------------------
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+
+struct VecBf16x8 {
+  static constexpr int kElems = 8;
+  using Raw = u32x4;
+  __device__ static Raw pad() { return Raw{0xFF80FF80u, 0xFF80FF80u, 0xFF80FF80u, 0xFF80FF80u}; }
+  __device__ static void unpack(const Raw& r, float (&x)[kElems]) {
+    x[0] = __uint_as_float(r.x << 16); x[1] = __uint_as_float(r.x & 0xFFFF0000u);
+    x[2] = __uint_as_float(r.y << 16); x[3] = __uint_as_float(r.y & 0xFFFF0000u);
+    x[4] = __uint_as_float(r.z << 16); x[5] = __uint_as_float(r.z & 0xFFFF0000u);
+    x[6] = __uint_as_float(r.w << 16); x[7] = __uint_as_float(r.w & 0xFFFF0000u);
+  }
+};
+struct VecF32x4 {
+  static constexpr int kElems = 4;
+  using Raw = u32x4;
+  __device__ static Raw pad() { return Raw{0xFF800000u, 0xFF800000u, 0xFF800000u, 0xFF800000u}; }
+  __device__ static void unpack(const Raw& r, float (&x)[kElems]) {
+    x[0] = __uint_as_float(r.x); x[1] = __uint_as_float(r.y);
+    x[2] = __uint_as_float(r.z); x[3] = __uint_as_float(r.w);
+  }
+};
+struct VecBf16x1 {
+  static constexpr int kElems = 1;
+  using Raw = unsigned short;
+  __device__ static Raw pad() { return (unsigned short)0xFF80u; }
+  __device__ static void unpack(const Raw& r, float (&x)[kElems]) { x[0] = __uint_as_float((unsigned)r << 16); }
+};
+struct VecF32x1 {
+  static constexpr int kElems = 1;
+  using Raw = unsigned int;
+  __device__ static Raw pad() { return 0xFF800000u; }
+  __device__ static void unpack(const Raw& r, float (&x)[kElems]) { x[0] = __uint_as_float(r); }
+};
+
+template <class Raw>
+__device__ __forceinline__ Raw load_stream(const Raw* p) {
+  return __builtin_nontemporal_load(p);
+}
+
+// ---------------------------------------------------------------------------
+// vocabulary pass over one wave's share of a row
+// ---------------------------------------------------------------------------
+struct WavePartial {
+  float m;    // maximum over the wave's elements (uniform)
+  float K;    // exp_ref(m) (uniform)
+  double S;   // sum of 2^(x log2e - K) over the wave's elements (uniform)
+  int first;  // lowest element index holding m (uniform)
+};
+
+constexpr int kAcc = 4;   // independent double accumulators per lane
+
+// The wave handles wave-loads k = w, w+S, w+2S, ... of the row (a wave-load
+// is 64 consecutive vectors); lane l reads vector k*64 + l.
+template <class Vec, int U, int S>
+__device__ WavePartial row_pass(const typename Vec::Raw* __restrict__ row, int nvec, int w) {
+  using Raw = typename Vec::Raw;
+  constexpr int E = Vec::kElems;
+  const int lane = lane_id();
+  const int nwl = (nvec + kWave - 1) / kWave;          // wave-loads in the row
+  const int nfull = nvec / kWave;                       // wave-loads with no padding
+  const int nj = nwl > w ? (nwl - w + S - 1) / S : 0;   // this wave's wave-loads
+  const int njf = nfull > w ? (nfull - w + S - 1) / S : 0;
+  const Raw* p = row + w * kWave + lane;
+  constexpr int kStride = S * kWave;
+
+  float m = kNegInf;
+  float K = kRefFloor;
+  double acc[kAcc];
+#pragma unroll
+  for (int a = 0; a < kAcc; ++a) acc[a] = 0.0;
+  int rec = -1;
+
+  auto consume = [&](const Raw (&r)[U], int batch) {
+    float x[U][E];
+#pragma unroll
+    for (int u = 0; u < U; ++u) Vec::unpack(r[u], x[u]);
+    float bm = kNegInf;
+#pragma unroll
+    for (int u = 0; u < U; ++u)
+#pragma unroll
+      for (int e = 0; e < E; ++e) bm = fmaxf(bm, x[u][e]);
+    rec = bm > m ? batch : rec;
+    const float mn = fmaxf(m, bm);
+    // a lane that has only seen padding keeps a finite reference, so that
+    // padding terms are exp2(-inf) = 0 rather than exp2(-inf + inf)
+    const float Kn = fmaxf(exp_ref(mn), kRefFloor);
+#pragma unroll
+    for (int a = 0; a < kAcc; ++a) acc[a] = rescale(acc[a], K, Kn);
+    m = mn;
+    K = Kn;
+#pragma unroll
+    for (int u = 0; u < U; ++u)
+#pragma unroll
+      for (int e = 0; e < E; ++e) acc[(u * E + e) % kAcc] += (double)term(x[u][e], K);
+  };
+
+  int j0 = 0;
+  for (; j0 + U <= njf; j0 += U) {
+    Raw r[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) r[u] = load_stream(p + (j0 + u) * kStride);
+    consume(r, j0 / U);
+  }
+  for (; j0 < nj; j0 += U) {
+    Raw r[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int j = j0 + u;
+      const int v = (w + j * S) * kWave + lane;
+      r[u] = (j < nj && v < nvec) ? load_stream(p + j * kStride) : Vec::pad();
+    }
+    consume(r, j0 / U);
+  }
+
+  // combine the lane accumulators (fixed order)
+  double s = (acc[0] + acc[1]) + (acc[2] + acc[3]);
+
+  WavePartial out;
+  out.m = wave_max(m);
+  // lowest index of the maximum: lanes holding it re-read their batch
+  int first = 0x7fffffff;
+  if (m == out.m && rec >= 0) {
+    for (int u = U - 1; u >= 0; --u) {
+      const int j = rec * U + u;
+      const int v = (w + j * S) * kWave + lane;
+      if (j < nj && v < nvec) {
+        float x[E];
+        Vec::unpack(row[v], x);
+#pragma unroll
+        for (int e = E - 1; e >= 0; --e)
+          if (x[e] == out.m) first = v * E + e;
+      }
+    }
+  }
+  out.first = wave_min(first);
+  // (K, S) across lanes
+  ks_step<0>(K, s);
+  ks_step<1>(K, s);
+  ks_step<2>(K, s);
+  ks_step<3>(K, s);
+  ks_step<4>(K, s);
+  {
+    float K0 = readlane_f32(K, 0), K1 = readlane_f32(K, 32);
+    double S0 = readlane_f64(s, 0), S1 = readlane_f64(s, 32);
+    ks_combine(K0, S0, K1, S1);
+    out.K = K0;
+    out.S = S0;
+  }
+  return out;
+}
+
+struct RowResult {
+  int token;
+  float conf, eps, lse;
+};
+
+// Final step of a row from its (m, K, S, first): s' = (S - e_M) / e_M with
+// e_M the greedy element's own term, recomputed exactly as it was summed.
+__device__ __forceinline__ RowResult finish_row(float M, float K, double S, int first) {
+  const float Kr = exp_ref(M);
+  const double eM = rescale((double)term(M, Kr), Kr, K);
+  const double sp = fmax((S - eM) / eM, 0.0);
+  RowResult r;
+  r.token = first;
+  r.conf = (float)(1.0 / (1.0 + sp));
+  r.eps = (float)(sp / (1.0 + sp));
+  r.lse = (float)((double)M + log1p(sp));
+  return r;
+}
+
+// ---------------------------------------------------------------------------
+// block bounds and candidates
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ bool window_ok(int s, int e, int L) {
+  return s >= 0 && s <= e && e <= L && e - s <= kMaxBlock;
+}
+
+struct RowOut {
+  int32_t* tokens;
+  float* conf;
+  float* eps;
+  float* lse;
+};
+
+__device__ __forceinline__ void store_row(const RowOut& o, size_t idx, const RowResult& r) {
+  if (o.tokens) o.tokens[idx] = r.token;
+  if (o.conf) o.conf[idx] = r.conf;
+  if (o.eps) o.eps[idx] = r.eps;
+  if (o.lse) o.lse[idx] = r.lse;
+}
+__device__ __forceinline__ void store_default(const RowOut& o, size_t idx) {
+  if (o.tokens) o.tokens[idx] = -1;
+  if (o.conf) o.conf[idx] = 0.0f;
+  if (o.eps) o.eps[idx] = 1.0f;
+  if (o.lse) o.lse[idx] = 0.0f;
+}
+
+// ---------------------------------------------------------------------------
+// kernel: vocabulary pass, S wavefronts per row, rows of all B*L slots
+// ---------------------------------------------------------------------------
+template <int S>
+struct SplitShape {
+  static constexpr int kWaves = S < 4 ? 4 : S;      // waves per workgroup
+  static constexpr int kRows = kWaves / S;          // rows per workgroup
+  static constexpr int kThreads = kWaves * kWave;
+};
+
+template <class Vec, int U, int S>
+__global__ void __launch_bounds__(SplitShape<S>::kThreads)
+k_confidence(const typename Vec::Raw* __restrict__ logits, int B, int L, int nvec,
+             const uint8_t* __restrict__ mask, const int32_t* __restrict__ bstart,
+             const int32_t* __restrict__ bend, RowOut out) {
+  using Shape = SplitShape<S>;
+  __shared__ WavePartial part[Shape::kWaves];
+  const int wave = threadIdx.x / kWave;
+  const int lane = threadIdx.x % kWave;
+  const int rloc = wave / S;
+  const int w = wave % S;
+  const long long slot = (long long)blockIdx.x * Shape::kRows + rloc;
+  const long long nslots = (long long)B * L;
+  bool cand = false;
+  int b = 0, i = 0;
+  if (slot < nslots) {
+    b = (int)(slot / L);
+    i = (int)(slot % L);
+    const int s = bstart[b], e = bend[b];
+    cand = window_ok(s, e, L) && i >= s && i < e && mask[slot] != 0;
+  }
+  WavePartial wp{};
+  if (cand) wp = row_pass<Vec, U, S>(logits + slot * (long long)nvec, nvec, w);
+  if constexpr (S > 1) {
+    if (lane == 0) part[wave] = wp;
+    __syncthreads();
+  }
+  if (w != 0 || lane != 0 || slot >= nslots) return;
+  if (!cand) {
+    store_default(out, (size_t)slot);
+    return;
+  }
+  float M = wp.m, K = wp.K;
+  double Ssum = wp.S;
+  int first = wp.first;
+  if constexpr (S > 1) {
+    M = part[rloc * S].m;
+#pragma unroll
+    for (int q = 1; q < S; ++q) M = fmaxf(M, part[rloc * S + q].m);
+    K = exp_ref(M);
+    Ssum = 0.0;
+    first = 0x7fffffff;
+#pragma unroll
+    for (int q = 0; q < S; ++q) {
+      const WavePartial& pq = part[rloc * S + q];
+      Ssum += rescale(pq.S, pq.K, K);
+      if (pq.m == M) first = min(first, pq.first);
+    }
+  }
+  store_row(out, (size_t)slot, finish_row(M, K, Ssum, first));
+}
+
+// ---------------------------------------------------------------------------
+// selection in one wavefront
+// ---------------------------------------------------------------------------
+enum Rule { kThreshold = 0, kFactor = 1, kProfile = 2 };
+
+__device__ __forceinline__ unsigned long long shfl_xor_u64(unsigned long long v, int mask) {
+  int lo = __shfl_xor((int)(v & 0xffffffffull), mask);
+  int hi = __shfl_xor((int)(v >> 32), mask);
+  return ((unsigned long long)(unsigned)hi << 32) | (unsigned)lo;
+}
+
+// Ascending bitonic sort of one 64-bit key per lane.
+__device__ __forceinline__ unsigned long long wave_sort(unsigned long long key, int lane) {
+#pragma unroll
+  for (int k = 2; k <= kWave; k <<= 1) {
+#pragma unroll
+    for (int j = k >> 1; j > 0; j >>= 1) {
+      const unsigned long long o = shfl_xor_u64(key, j);
+      const bool up = (lane & k) == 0;
+      const bool low = (lane & j) == 0;
+      const unsigned long long lo = key < o ? key : o;
+      const unsigned long long hi = key < o ? o : key;
+      key = (low == up) ? lo : hi;
+    }
+  }
+  return key;
+}
+
+__device__ __forceinline__ double shfl_up_f64(double v, int d) {
+  long long b = __double_as_longlong(v);
+  int lo = __shfl_up((int)(b & 0xffffffffll), d);
+  int hi = __shfl_up((int)(b >> 32), d);
+  return __longlong_as_double(((long long)hi << 32) | (unsigned int)lo);
+}
+
+__device__ __forceinline__ double shfl_f64(double v, int src) {
+  long long b = __double_as_longlong(v);
+  int lo = __shfl((int)(b & 0xffffffffll), src);
+  int hi = __shfl((int)(b >> 32), src);
+  return __longlong_as_double(((long long)hi << 32) | (unsigned int)lo);
+}
+
+// Inclusive prefix sum across the wave, fixed order.
+__device__ __forceinline__ double wave_scan_f64(double v, int lane) {
+#pragma unroll
+  for (int d = 1; d < kWave; d <<= 1) {
+    const double o = shfl_up_f64(v, d);
+    if (lane >= d) v += o;
+  }
+  return v;
+}
+
+// Decides the commit set of one block.  Lane j describes slot j of the block
+// (position start + j): `valid` marks a candidate, `key` orders candidates by
+// confidence descending (smaller key = more confident), `e` is the candidate's
+// eps = 1 - c in double and `conf` its confidence (threshold rule only).
+// Returns n* (the number of commits) and sets `commit_slot` for lane j's slot.
+template <int R>
+__device__ int select_wave(bool valid, unsigned key, double e, float conf, float param,
+                           bool& commit_slot) {
+  const int lane = lane_id();
+  const unsigned long long vmask = __ballot(valid);
+  const int m = __popcll(vmask);
+  // [invalid:1][key:32][slot:6]: candidates first, by key, ties by position
+  const unsigned long long k64 = ((unsigned long long)(valid ? 0u : 1u) << 63) |
+                                 ((unsigned long long)key << 6) | (unsigned)lane;
+  const unsigned long long sk = wave_sort(k64, lane);
+  const int rank_slot = (int)(sk & 63u);   // slot held by sorted rank `lane`
+  const bool rvalid = lane < m;
+  bool take;
+  int nstar;
+  if constexpr (R == kThreshold) {
+    const float c = __shfl(conf, rank_slot);
+    const bool pass = rvalid && c >= param;
+    const unsigned long long pm = __ballot(pass);
+    if (pm != 0ull) {
+      take = pass;
+      nstar = __popcll(pm);
+    } else {
+      take = rvalid && lane == 0;
+      nstar = m > 0 ? 1 : 0;
+    }
+  } else {
+    const double es = shfl_f64(e, rank_slot);               // eps_(n), n = lane + 1
+    const double ep = shfl_up_f64(es, 1);
+    double lhs = (double)(lane + 2) * es;                   // (n+1) eps_(n)
+    if constexpr (R == kProfile) {
+      const double t = (rvalid && lane >= 1) ? (double)lane * (es - ep) : 0.0;
+      lhs -= wave_scan_f64(t, lane);                        // minus B_n
+    }
+    const bool acc = rvalid && lhs < (double)param;
+    const unsigned long long am = __ballot(acc);
+    nstar = am ? 64 - __clzll((long long)am) : (m > 0 ? 1 : 0);
+    take = lane < nstar;
+  }
+  // route rank decisions back to slots (rank_slot is a permutation of 0..63)
+  const int routed = __builtin_amdgcn_ds_permute(rank_slot * 4, take ? 1 : 0);
+  commit_slot = routed != 0;
+  return nstar;
+}
+
+// Sort key and eps of a candidate from float eps (preferred) or conf only.
+__device__ __forceinline__ void cand_key(const float* eps_arr, float c, size_t idx, unsigned& key,
+                                         double& e) {
+  if (eps_arr) {
+    const float ev = eps_arr[idx];
+    key = __float_as_uint(ev);          // eps >= 0: bit order is value order
+    e = (double)ev;
+  } else {
+    key = ~__float_as_uint(c);          // c >= 0: descending c = ascending ~bits
+    e = 1.0 - (double)c;                // exact in double
+  }
+}
+
+struct SelectIO {
+  const float* conf;
+  const float* eps;           // may be null
+  uint8_t* mask;              // read; cleared at commits when reveal
+  const int32_t* bstart;
+  const int32_t* bend;
+  uint8_t* commit;            // may be null
+  int32_t* n_commit;          // may be null
+  const int32_t* tokens;      // reveal source (may be null: no reveal)
+  int32_t* x;                 // reveal target (may be null: no reveal)
+};
+
+template <int R>
+__global__ void __launch_bounds__(256) k_select(SelectIO io, int B, int L, float param) {
+  const int lane = threadIdx.x % kWave;
+  const int b = blockIdx.x * 4 + threadIdx.x / kWave;
+  if (b >= B) return;
+  const size_t row = (size_t)b * L;
+  const int s = io.bstart[b], e_end = io.bend[b];
+  const bool ok = window_ok(s, e_end, L);
+  const int i = s + lane;
+  const bool inwin = ok && lane < e_end - s;
+  const bool valid = inwin && io.mask[row + i] != 0;
+  float c = 0.0f;
+  unsigned key = 0xFFFFFFFFu;
+  double e = 1.0;
+  if (valid) {
+    c = io.conf[row + i];
+    cand_key(io.eps, c, row + i, key, e);
+  }
+  bool take = false;
+  const int nstar = select_wave<R>(valid, key, e, c, param, take);
+  if (io.commit) {
+    // every entry of row b written once: window slots by their lane, the rest zero
+    for (int q = lane; q < L; q += kWave)
+      if (!(ok && q >= s && q < e_end)) io.commit[row + q] = 0;
+    if (inwin) io.commit[row + i] = take ? 1 : 0;
+  }
+  if (take && io.x) {
+    io.x[row + i] = io.tokens[row + i];
+    io.mask[row + i] = 0;
+  }
+  if (io.n_commit && lane == 0) io.n_commit[b] = ok ? nstar : -1;
+}
+
+// ---------------------------------------------------------------------------
+// kernel: fused decode step, one workgroup of W waves per sequence
+// ---------------------------------------------------------------------------
+template <class Vec, int U, int W, int R>
+__global__ void __launch_bounds__(W * kWave)
+k_fused(const typename Vec::Raw* __restrict__ logits, int B, int L, int nvec,
+        uint8_t* __restrict__ mask, const int32_t* __restrict__ bstart,
+        const int32_t* __restrict__ bend, int32_t* __restrict__ x, float param, RowOut out,
+        uint8_t* __restrict__ commit, int32_t* __restrict__ n_commit) {
+  __shared__ int s_cand[kMaxBlock];       // candidate slots, compacted
+  __shared__ int s_tok[kMaxBlock];
+  __shared__ float s_conf[kMaxBlock];
+  __shared__ float s_eps[kMaxBlock];
+  __shared__ int s_m;
+  const int b = blockIdx.x;
+  const int wave = threadIdx.x / kWave;
+  const int lane = threadIdx.x % kWave;
+  const size_t row0 = (size_t)b * L;
+  const int s = bstart[b], e = bend[b];
+  const bool ok = window_ok(s, e, L);
+  const int len = ok ? e - s : 0;
+  if (wave == 0) {
+    const bool valid = lane < len && mask[row0 + s + lane] != 0;
+    const unsigned long long vm = __ballot(valid);
+    const int before = __popcll(vm & ((1ull << lane) - 1ull));
+    if (valid) s_cand[before] = lane;
+    if (lane == 0) s_m = __popcll(vm);
+  }
+  // default outputs for every non-candidate row of this sequence
+  for (int q = threadIdx.x; q < L; q += W * kWave) {
+    const bool inwin = q >= s && q < s + len;
+    if (!inwin || mask[row0 + q] == 0) {
+      store_default(out, row0 + q);
+      if (commit) commit[row0 + q] = 0;
+    }
+  }
+  __syncthreads();
+  const int m = s_m;
+  for (int c = wave; c < m; c += W) {
+    const int slot = s_cand[c];
+    const size_t r = row0 + s + slot;
+    const WavePartial wp = row_pass<Vec, U, 1>(logits + r * (size_t)nvec, nvec, 0);
+    const RowResult rr = finish_row(wp.m, wp.K, wp.S, wp.first);
+    if (lane == 0) {
+      store_row(out, r, rr);
+      s_tok[slot] = rr.token;
+      s_conf[slot] = rr.conf;
+      s_eps[slot] = rr.eps;
+    }
+  }
+  __syncthreads();
+  if (wave != 0) return;
+  const bool valid = lane < len && mask[row0 + s + lane] != 0;
+  const float ev = valid ? s_eps[lane] : 1.0f;
+  bool take = false;
+  const int nstar = select_wave<R>(valid, __float_as_uint(ev), (double)ev,
+                                   valid ? s_conf[lane] : 0.0f, param, take);
+  if (valid) {
+    if (commit) commit[row0 + s + lane] = take ? 1 : 0;
+    if (take) {
+      x[row0 + s + lane] = s_tok[lane];
+      mask[row0 + s + lane] = 0;
+    }
+  }
+  if (n_commit && lane == 0) n_commit[b] = ok ? nstar : -1;
+}
+
+__global__ void __launch_bounds__(256) k_reveal(const uint8_t* __restrict__ commit,
+                                                 const int32_t* __restrict__ tokens,
+                                                 int32_t* __restrict__ x, uint8_t* __restrict__ mask,
+                                                 long long n) {
+  for (long long k = (long long)blockIdx.x * blockDim.x + threadIdx.x; k < n;
+       k += (long long)gridDim.x * blockDim.x) {
+    if (commit[k]) {
+      x[k] = tokens[k];
+      mask[k] = 0;
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// host side: planning and launches
+// ---------------------------------------------------------------------------
+struct Plan {
+  bool fused;   // one workgroup per sequence, selection in the same kernel
+  int split;    // wavefronts per row in the confidence kernel
+  int U;        // vectors per lane per batch
+};
+
+constexpr int kFusedMinB = 128;
+constexpr int kFusedWaves = 8;
+constexpr int kTargetWaves = 2048;   // 8 per CU on 256 CUs
+
+static Plan make_plan(int B, int L, int V, fdllm_dtype dt) {
+  (void)V;
+  (void)dt;
+  Plan p{};
+  const long long win = L < kMaxBlock ? L : kMaxBlock;
+  p.fused = B >= kFusedMinB;
+  p.split = 1;
+  if (!p.fused) {
+    long long slots = (long long)B * win;
+    while (p.split < 16 && slots * p.split < kTargetWaves) p.split <<= 1;
+  }
+  p.U = 8;
+  return p;
+}
+
+static bool vec_path(const void* logits, int V, fdllm_dtype dt) {
+  const int per = dt == FDLLM_BF16 ? 8 : 4;
+  return V % per == 0 && ((uintptr_t)logits % 16) == 0;
+}
+
+template <class Vec>
+static hipError_t launch_confidence_t(const void* logits, int B, int L, int nvec, int split,
+                                      const uint8_t* mask, const int32_t* bs, const int32_t* be,
+                                      RowOut out, hipStream_t st) {
+  const long long nslots = (long long)B * L;
+  const auto* lg = (const typename Vec::Raw*)logits;
+#define FDLLM_CONF_CASE(SPLIT)                                                                  \
+  case SPLIT: {                                                                                 \
+    using Sh = SplitShape<SPLIT>;                                                               \
+    const long long grid = (nslots + Sh::kRows - 1) / Sh::kRows;                                \
+    hipLaunchKernelGGL((k_confidence<Vec, 8, SPLIT>), dim3((unsigned)grid), dim3(Sh::kThreads), \
+                       0, st, lg, B, L, nvec, mask, bs, be, out);                               \
+    break;                                                                                      \
+  }
+  switch (split) {
+    FDLLM_CONF_CASE(1)
+    FDLLM_CONF_CASE(2)
+    FDLLM_CONF_CASE(4)
+    FDLLM_CONF_CASE(8)
+    FDLLM_CONF_CASE(16)
+    default:
+      return hipErrorInvalidValue;
+  }
+#undef FDLLM_CONF_CASE
+  return hipGetLastError();
+}
+
+static hipError_t launch_confidence(const void* logits, fdllm_dtype dt, int B, int L, int V,
+                                    int split, const uint8_t* mask, const int32_t* bs,
+                                    const int32_t* be, RowOut out, hipStream_t st) {
+  if (vec_path(logits, V, dt)) {
+    if (dt == FDLLM_BF16)
+      return launch_confidence_t<VecBf16x8>(logits, B, L, V / 8, split, mask, bs, be, out, st);
+    return launch_confidence_t<VecF32x4>(logits, B, L, V / 4, split, mask, bs, be, out, st);
+  }
+  if (dt == FDLLM_BF16)
+    return launch_confidence_t<VecBf16x1>(logits, B, L, V, split, mask, bs, be, out, st);
+  return launch_confidence_t<VecF32x1>(logits, B, L, V, split, mask, bs, be, out, st);
+}
+
+static hipError_t launch_select(fdllm_selector sel, const SelectIO& io, int B, int L, float param,
+                                hipStream_t st) {
+  const dim3 grid((unsigned)((B + 3) / 4)), block(256);
+  switch (sel) {
+    case FDLLM_SEL_THRESHOLD:
+      hipLaunchKernelGGL(k_select<kThreshold>, grid, block, 0, st, io, B, L, param);
+      break;
+    case FDLLM_SEL_FACTOR:
+      hipLaunchKernelGGL(k_select<kFactor>, grid, block, 0, st, io, B, L, param);
+      break;
+    default:
+      hipLaunchKernelGGL(k_select<kProfile>, grid, block, 0, st, io, B, L, param);
+      break;
+  }
+  return hipGetLastError();
+}
+
+template <class Vec, int R>
+static void launch_fused_t(const void* logits, int B, int L, int nvec, uint8_t* mask,
+                           const int32_t* bs, const int32_t* be, int32_t* x, float param,
+                           RowOut out, uint8_t* commit, int32_t* n_commit, hipStream_t st) {
+  hipLaunchKernelGGL((k_fused<Vec, 8, kFusedWaves, R>), dim3((unsigned)B), dim3(kFusedWaves * kWave),
+                     0, st, (const typename Vec::Raw*)logits, B, L, nvec, mask, bs, be, x, param,
+                     out, commit, n_commit);
+}
+
+template <class Vec>
+static hipError_t launch_fused_v(fdllm_selector sel, const void* logits, int B, int L, int nvec,
+                                 uint8_t* mask, const int32_t* bs, const int32_t* be, int32_t* x,
+                                 float param, RowOut out, uint8_t* commit, int32_t* n_commit,
+                                 hipStream_t st) {
+  switch (sel) {
+    case FDLLM_SEL_THRESHOLD:
+      launch_fused_t<Vec, kThreshold>(logits, B, L, nvec, mask, bs, be, x, param, out, commit, n_commit, st);
+      break;
+    case FDLLM_SEL_FACTOR:
+      launch_fused_t<Vec, kFactor>(logits, B, L, nvec, mask, bs, be, x, param, out, commit, n_commit, st);
+      break;
+    default:
+      launch_fused_t<Vec, kProfile>(logits, B, L, nvec, mask, bs, be, x, param, out, commit, n_commit, st);
+      break;
+  }
+  return hipGetLastError();
+}
+
+static hipError_t launch_fused(fdllm_selector sel, const void* logits, fdllm_dtype dt, int B, int L,
+                               int V, uint8_t* mask, const int32_t* bs, const int32_t* be,
+                               int32_t* x, float param, RowOut out, uint8_t* commit,
+                               int32_t* n_commit, hipStream_t st) {
+  if (vec_path(logits, V, dt)) {
+    if (dt == FDLLM_BF16)
+      return launch_fused_v<VecBf16x8>(sel, logits, B, L, V / 8, mask, bs, be, x, param, out, commit, n_commit, st);
+    return launch_fused_v<VecF32x4>(sel, logits, B, L, V / 4, mask, bs, be, x, param, out, commit, n_commit, st);
+  }
+  if (dt == FDLLM_BF16)
+    return launch_fused_v<VecBf16x1>(sel, logits, B, L, V, mask, bs, be, x, param, out, commit, n_commit, st);
+  return launch_fused_v<VecF32x1>(sel, logits, B, L, V, mask, bs, be, x, param, out, commit, n_commit, st);
+}
+
+static bool sizes_ok(int B, int L, int V) {
+  if (B < 0 || L < 1 || V < 1) return false;
+  const long double total = (long double)B * (long double)L * (long double)V;
+  return total < 4.0e18L;
+}
+
+static size_t align256(size_t n) { return (n + 255) & ~(size_t)255; }
+
+static size_t workspace_bytes_for(int B, int L, const Plan& p) {
+  if (p.fused) return 0;
+  const size_t n = (size_t)B * (size_t)L;
+  return 3 * align256(n * 4);
+}
+
+}  // namespace fdllm
+
+using namespace fdllm;
+
+extern "C" {
+
+const char* fdllm_status_string(fdllm_status st) {
+  switch (st) {
+    case FDLLM_OK: return "ok";
+    case FDLLM_ERR_INVALID_ARG: return "invalid argument (null pointer, negative size or bad enum)";
+    case FDLLM_ERR_UNSUPPORTED_DTYPE: return "unsupported logits dtype";
+    case FDLLM_ERR_SIZE: return "unsupported size (V < 1 or too many elements)";
+    case FDLLM_ERR_WORKSPACE: return "workspace missing or too small";
+    case FDLLM_ERR_HIP: return "HIP runtime error at launch";
+    default: return "unknown status";
+  }
+}
+
+fdllm_status fdllm_workspace_size(int B, int L, int V, fdllm_dtype dtype, size_t* bytes) {
+  if (!bytes) return FDLLM_ERR_INVALID_ARG;
+  if (dtype != FDLLM_BF16 && dtype != FDLLM_F32) return FDLLM_ERR_UNSUPPORTED_DTYPE;
+  if (B < 0 || L < 1) return FDLLM_ERR_INVALID_ARG;
+  if (!sizes_ok(B, L, V)) return FDLLM_ERR_SIZE;
+  *bytes = workspace_bytes_for(B, L, make_plan(B, L, V, dtype));
+  return FDLLM_OK;
+}
+
+fdllm_status fdllm_confidence(const void* logits, fdllm_dtype dtype, int B, int L, int V,
+                              const uint8_t* mask, const int32_t* block_start,
+                              const int32_t* block_end, int32_t* tokens, float* conf, float* eps,
+                              float* lse, fdllm_stream stream) {
+  if (dtype != FDLLM_BF16 && dtype != FDLLM_F32) return FDLLM_ERR_UNSUPPORTED_DTYPE;
+  if (B < 0 || L < 1) return FDLLM_ERR_INVALID_ARG;
+  if (!sizes_ok(B, L, V)) return FDLLM_ERR_SIZE;
+  if (B == 0) return FDLLM_OK;
+  if (!logits || !mask || !block_start || !block_end || !tokens || !conf) return FDLLM_ERR_INVALID_ARG;
+  const Plan p = make_plan(B, L, V, dtype);
+  RowOut out{tokens, conf, eps, lse};
+  hipError_t err = launch_confidence(logits, dtype, B, L, V, p.split, mask, block_start, block_end,
+                                     out, (hipStream_t)stream);
+  return err == hipSuccess ? FDLLM_OK : FDLLM_ERR_HIP;
+}
+
+static fdllm_status select_common(fdllm_selector sel, const float* conf, const float* eps,
+                                  const uint8_t* mask, const int32_t* bs, const int32_t* be, int B,
+                                  int L, float param, uint8_t* commit, int32_t* n_commit,
+                                  fdllm_stream stream) {
+  if (B < 0 || L < 1) return FDLLM_ERR_INVALID_ARG;
+  if (B == 0) return FDLLM_OK;
+  if (!conf || !mask || !bs || !be || !commit) return FDLLM_ERR_INVALID_ARG;
+  SelectIO io{conf, eps, const_cast<uint8_t*>(mask), bs, be, commit, n_commit, nullptr, nullptr};
+  hipError_t err = launch_select(sel, io, B, L, param, (hipStream_t)stream);
+  return err == hipSuccess ? FDLLM_OK : FDLLM_ERR_HIP;
+}
+
+fdllm_status fdllm_select_profile(const float* conf, const float* eps, const uint8_t* mask,
+                                  const int32_t* block_start, const int32_t* block_end, int B,
+                                  int L, float f, uint8_t* commit, int32_t* n_commit,
+                                  fdllm_stream stream) {
+  return select_common(FDLLM_SEL_PROFILE, conf, eps, mask, block_start, block_end, B, L, f, commit,
+                       n_commit, stream);
+}
+
+fdllm_status fdllm_select_factor(const float* conf, const float* eps, const uint8_t* mask,
+                                 const int32_t* block_start, const int32_t* block_end, int B,
+                                 int L, float f, uint8_t* commit, int32_t* n_commit,
+                                 fdllm_stream stream) {
+  return select_common(FDLLM_SEL_FACTOR, conf, eps, mask, block_start, block_end, B, L, f, commit,
+                       n_commit, stream);
+}
+
+fdllm_status fdllm_select_threshold(const float* conf, const float* eps, const uint8_t* mask,
+                                    const int32_t* block_start, const int32_t* block_end, int B,
+                                    int L, float tau, uint8_t* commit, int32_t* n_commit,
+                                    fdllm_stream stream) {
+  return select_common(FDLLM_SEL_THRESHOLD, conf, eps, mask, block_start, block_end, B, L, tau,
+                       commit, n_commit, stream);
+}
+
+fdllm_status fdllm_reveal(const uint8_t* commit, const int32_t* tokens, int32_t* x, uint8_t* mask,
+                          int B, int L, fdllm_stream stream) {
+  if (B < 0 || L < 1) return FDLLM_ERR_INVALID_ARG;
+  if (B == 0) return FDLLM_OK;
+  if (!commit || !tokens || !x || !mask) return FDLLM_ERR_INVALID_ARG;
+  const long long n = (long long)B * L;
+  long long grid = (n + 255) / 256;
+  if (grid > 65536) grid = 65536;
+  hipLaunchKernelGGL(k_reveal, dim3((unsigned)grid), dim3(256), 0, (hipStream_t)stream, commit,
+                     tokens, x, mask, n);
+  return hipGetLastError() == hipSuccess ? FDLLM_OK : FDLLM_ERR_HIP;
+}
+
+fdllm_status fdllm_decode_step(const void* logits, fdllm_dtype dtype, int B, int L, int V,
+                               uint8_t* mask, const int32_t* block_start, const int32_t* block_end,
+                               int32_t* x, fdllm_selector sel, float param, int32_t* tokens,
+                               float* conf, float* eps, float* lse, uint8_t* commit,
+                               int32_t* n_commit, void* workspace, size_t workspace_bytes,
+                               fdllm_stream stream) {
+  if (dtype != FDLLM_BF16 && dtype != FDLLM_F32) return FDLLM_ERR_UNSUPPORTED_DTYPE;
+  if (sel != FDLLM_SEL_THRESHOLD && sel != FDLLM_SEL_FACTOR && sel != FDLLM_SEL_PROFILE)
+    return FDLLM_ERR_INVALID_ARG;
+  if (B < 0 || L < 1) return FDLLM_ERR_INVALID_ARG;
+  if (!sizes_ok(B, L, V)) return FDLLM_ERR_SIZE;
+  if (B == 0) return FDLLM_OK;
+  if (!logits || !mask || !block_start || !block_end || !x) return FDLLM_ERR_INVALID_ARG;
+  const Plan p = make_plan(B, L, V, dtype);
+  hipStream_t st = (hipStream_t)stream;
+  RowOut out{tokens, conf, eps, lse};
+  hipError_t err;
+  if (p.fused) {
+    err = launch_fused(sel, logits, dtype, B, L, V, mask, block_start, block_end, x, param, out,
+                       commit, n_commit, st);
+    return err == hipSuccess ? FDLLM_OK : FDLLM_ERR_HIP;
+  }
+  // two kernels: confidence into the caller's arrays or the workspace, then select+reveal
+  const size_t n = (size_t)B * (size_t)L;
+  const bool need_ws = !tokens || !conf || !eps;
+  if (need_ws && (!workspace || workspace_bytes < workspace_bytes_for(B, L, p)))
+    return FDLLM_ERR_WORKSPACE;
+  char* ws = (char*)workspace;
+  if (!tokens) tokens = (int32_t*)ws;
+  if (!conf) conf = (float*)(ws + align256(n * 4));
+  if (!eps) eps = (float*)(ws + 2 * align256(n * 4));
+  out = RowOut{tokens, conf, eps, lse};
+  err = launch_confidence(logits, dtype, B, L, V, p.split, mask, block_start, block_end, out, st);
+  if (err != hipSuccess) return FDLLM_ERR_HIP;
+  SelectIO io{conf, eps, mask, block_start, block_end, commit, n_commit, tokens, x};
+  err = launch_select(sel, io, B, L, param, st);
+  return err == hipSuccess ? FDLLM_OK : FDLLM_ERR_HIP;
+}
+
+}  // extern "C"

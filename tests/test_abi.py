@@ -1,0 +1,105 @@
+"""The C-ABI library loads, exports what include/fdllm.h declares, and its
+host-side argument checks reject bad calls without touching a GPU."""
+import ctypes
+import os
+import re
+
+import pytest
+
+import paper_2606_02955_amd as fd
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "fdllm.h")
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(fdllm_[a-z_]+)\s*\(", text)))
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(fd.LIB_PATH):
+        from paper_2606_02955_amd import build
+        build.build()
+    return fd.load()
+
+
+def test_every_declared_symbol_is_exported(lib):
+    names = declared_functions()
+    assert set(names) == set(fd.EXPORTS), names
+    for n in names:
+        assert hasattr(lib, n), n
+
+
+def test_status_strings(lib):
+    for st in (0, -1, -2, -3, -4, -5):
+        assert len(fd.status_string(st)) > 0
+    assert fd.status_string(0) == "ok"
+    assert "unknown" in fd.status_string(99)
+
+
+def test_workspace_size_host_only(lib):
+    n = ctypes.c_size_t(123)
+    assert lib.fdllm_workspace_size(1024, 32, 126464, 0, ctypes.byref(n)) == 0
+    assert n.value == 0                      # large batches run fused: no workspace
+    assert lib.fdllm_workspace_size(8, 32, 126464, 0, ctypes.byref(n)) == 0
+    assert n.value >= 3 * 8 * 32 * 4
+    assert lib.fdllm_workspace_size(8, 32, 126464, 7, ctypes.byref(n)) == fd.ERR_UNSUPPORTED_DTYPE
+    assert lib.fdllm_workspace_size(8, 32, 0, 0, ctypes.byref(n)) == fd.ERR_SIZE
+    assert lib.fdllm_workspace_size(-1, 32, 10, 0, ctypes.byref(n)) == fd.ERR_INVALID_ARG
+    assert lib.fdllm_workspace_size(8, 32, 10, 0, None) == fd.ERR_INVALID_ARG
+
+
+def test_error_paths_enqueue_nothing(lib):
+    p = ctypes.c_void_p(0x1000)            # never dereferenced: checks fail first
+    null = None
+    # confidence: null logits / tokens / conf, bad dtype, bad sizes
+    assert lib.fdllm_confidence(null, 0, 2, 4, 16, p, p, p, p, p, null, null, null) == fd.ERR_INVALID_ARG
+    assert lib.fdllm_confidence(p, 0, 2, 4, 16, p, p, p, null, p, null, null, null) == fd.ERR_INVALID_ARG
+    assert lib.fdllm_confidence(p, 0, 2, 4, 16, p, p, p, p, null, null, null, null) == fd.ERR_INVALID_ARG
+    assert lib.fdllm_confidence(p, 5, 2, 4, 16, p, p, p, p, p, null, null, null) == fd.ERR_UNSUPPORTED_DTYPE
+    assert lib.fdllm_confidence(p, 0, 2, 4, 0, p, p, p, p, p, null, null, null) == fd.ERR_SIZE
+    assert lib.fdllm_confidence(p, 0, -2, 4, 16, p, p, p, p, p, null, null, null) == fd.ERR_INVALID_ARG
+    assert lib.fdllm_confidence(p, 0, 2, 0, 16, p, p, p, p, p, null, null, null) == fd.ERR_INVALID_ARG
+    assert lib.fdllm_confidence(p, 0, 1 << 30, 1 << 30, 1 << 30, p, p, p, p, p, null, null, null) == fd.ERR_SIZE
+    # B == 0 is a no-op
+    assert lib.fdllm_confidence(null, 0, 0, 4, 16, null, null, null, null, null, null, null, null) == 0
+    # selectors: conf, mask, bounds and commit are required
+    for name in ("fdllm_select_profile", "fdllm_select_factor", "fdllm_select_threshold"):
+        f = getattr(lib, name)
+        assert f(null, null, p, p, p, 2, 4, 1.0, p, null, null) == fd.ERR_INVALID_ARG
+        assert f(p, null, p, p, p, 2, 4, 1.0, null, null, null) == fd.ERR_INVALID_ARG
+        assert f(p, null, null, p, p, 2, 4, 1.0, p, null, null) == fd.ERR_INVALID_ARG
+        assert f(p, null, p, p, p, 2, 0, 1.0, p, null, null) == fd.ERR_INVALID_ARG
+        assert f(null, null, null, null, null, 0, 4, 1.0, null, null, null) == 0
+    assert lib.fdllm_reveal(null, p, p, p, 2, 4, null) == fd.ERR_INVALID_ARG
+    assert lib.fdllm_reveal(p, p, p, p, -1, 4, null) == fd.ERR_INVALID_ARG
+    # decode step: bad selector, dtype, null in/out arrays, missing workspace
+    args = lambda **kw: [kw.get("logits", p), kw.get("dt", 0), kw.get("B", 8), 32, kw.get("V", 64),
+                         kw.get("mask", p), p, p, kw.get("x", p), kw.get("sel", 2), 1.0,
+                         null, null, null, null, null, null, kw.get("ws", null), kw.get("wsb", 0), null]
+    assert lib.fdllm_decode_step(*args(sel=3)) == fd.ERR_INVALID_ARG
+    assert lib.fdllm_decode_step(*args(dt=9)) == fd.ERR_UNSUPPORTED_DTYPE
+    assert lib.fdllm_decode_step(*args(logits=null)) == fd.ERR_INVALID_ARG
+    assert lib.fdllm_decode_step(*args(mask=null)) == fd.ERR_INVALID_ARG
+    assert lib.fdllm_decode_step(*args(x=null)) == fd.ERR_INVALID_ARG
+    assert lib.fdllm_decode_step(*args(V=0)) == fd.ERR_SIZE
+    assert lib.fdllm_decode_step(*args()) == fd.ERR_WORKSPACE            # B=8: two-kernel plan
+    assert lib.fdllm_decode_step(*args(ws=p, wsb=16)) == fd.ERR_WORKSPACE
+
+
+def test_binding_refuses_cpu_tensors(lib):
+    import torch
+    lg = torch.zeros(1, 2, 8, dtype=torch.bfloat16)
+    m = torch.ones(1, 2, dtype=torch.uint8)
+    b = torch.zeros(1, dtype=torch.int32)
+    with pytest.raises(ValueError):
+        fd.fdllm_confidence(lg, m, b, b + 2, torch.zeros(1, 2, dtype=torch.int32),
+                            torch.zeros(1, 2))
+
+
+def test_missing_library_fails_loudly(tmp_path):
+    with pytest.raises(FileNotFoundError):
+        fd.load(str(tmp_path / "libfdllm.so"))

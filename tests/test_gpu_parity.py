@@ -1,0 +1,189 @@
+"""GPU parity: the HIP path against the CPU oracle on the same seeded inputs.
+
+Level 1: per-position outputs of fdllm_confidence vs the oracle.
+Level 2: fdllm_select_* vs the oracle's rules fed the GPU's own conf/eps.
+Level 3: fdllm_decode_step end to end vs the oracle's decode step.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import workloads
+from parity import (say, row_source, candidates, compare_rows, gpu_confidence,
+                    oracle_confidence_subset, check_defaults, compare_selection)
+
+pytestmark = pytest.mark.gpu
+
+RULES = [("profile", 1.0), ("profile", 0.75), ("profile", 2.0), ("factor", 1.0),
+         ("factor", 0.75), ("threshold", 0.9)]
+
+SMALL = [
+    # (B, L, V, dtype, window)  -- vector and scalar paths, ragged wave-loads
+    (3, 20, 16, torch.bfloat16, None),
+    (2, 9, 13, torch.bfloat16, None),
+    (4, 40, 1000, torch.bfloat16, None),
+    (2, 70, 5003, torch.float32, None),
+    (5, 8, 8200, torch.bfloat16, None),
+    (3, 33, 126464, torch.bfloat16, 33),
+    (2, 17, 126464, torch.float32, 17),
+    (2, 64, 6000, torch.float32, 64),
+    (130, 8, 520, torch.bfloat16, None),      # enough sequences for the fused plan
+    (160, 12, 1024, torch.float32, 12),
+    (129, 3, 7, torch.bfloat16, None),        # fused plan, scalar path
+]
+
+
+def _case(B, L, V, dt, window, seed=0):
+    return workloads.random_case(B, L, V, dt, device="cuda", seed=seed, window=window)
+
+
+@pytest.mark.parametrize("B,L,V,dt,window", SMALL)
+def test_confidence_vs_oracle(gpu, B, L, V, dt, window):
+    inp = _case(B, L, V, dt, window, seed=B * 7 + L)
+    say(f"[confidence] {inp.name}")
+    g = [t.cpu().numpy() for t in gpu_confidence(gpu, inp)]
+    o = oracle_confidence_subset(inp, range(B))
+    mask, start, end = inp.mask.cpu().numpy(), inp.start.cpu().numpy(), inp.end.cpu().numpy()
+    cells = candidates(mask, start, end, range(B))
+    worst = compare_rows(*g, *o, cells)
+    check_defaults(*g, mask, start, end, range(B))
+    say(f"  {len(cells)} rows, worst rel err {worst}")
+
+
+@pytest.mark.parametrize("B,L,V,dt,window", SMALL[:6] + SMALL[8:9])
+def test_select_vs_oracle_on_gpu_confidences(gpu, B, L, V, dt, window):
+    inp = _case(B, L, V, dt, window, seed=B * 11 + L)
+    say(f"[select] {inp.name}")
+    tok, conf, eps, lse = gpu_confidence(gpu, inp)
+    mask, start, end = inp.mask.cpu().numpy(), inp.start.cpu().numpy(), inp.end.cpu().numpy()
+    for use_eps in (True, False):
+        e_in = eps if use_eps else None
+        e_or = eps.double().cpu().numpy() if use_eps else 1.0 - conf.double().cpu().numpy()
+        for rule, p in RULES:
+            commit = torch.full((B, L), 9, dtype=torch.uint8, device="cuda")
+            n = torch.full((B,), -9, dtype=torch.int32, device="cuda")
+            gpu.select(rule, conf, e_in, inp.mask, inp.start, inp.end, p, commit, n)
+            torch.cuda.synchronize()
+            oc, on, flagged, _ = oracle.select(e_or, conf.double().cpu().numpy(), mask, start, end, rule, p)
+            nf, nfm = compare_selection(commit.cpu().numpy(), n.cpu().numpy(), oc, on, flagged, range(B))
+            say(f"  {rule}({p}) eps={'gpu' if use_eps else '1-conf'}: flagged {nf} (matching {nfm})")
+
+
+def _decode(gpu, inp, rule, p, with_outputs=True):
+    B, L, V = inp.logits.shape
+    d = "cuda"
+    mask, x = inp.mask.clone(), inp.x.clone()
+    outs = dict(tokens=torch.full((B, L), -7, dtype=torch.int32, device=d),
+                conf=torch.full((B, L), -7.0, device=d), eps=torch.full((B, L), -7.0, device=d),
+                lse=torch.full((B, L), -7.0, device=d),
+                commit=torch.full((B, L), 9, dtype=torch.uint8, device=d),
+                n_commit=torch.full((B,), -9, dtype=torch.int32, device=d))
+    if not with_outputs:
+        outs = dict(commit=outs["commit"], n_commit=outs["n_commit"])
+    gpu.fdllm_decode_step(inp.logits, mask, inp.start, inp.end, x, rule, p, **outs)
+    torch.cuda.synchronize()
+    return mask, x, outs
+
+
+@pytest.mark.parametrize("B,L,V,dt,window", SMALL)
+def test_decode_step_vs_oracle(gpu, B, L, V, dt, window):
+    inp = _case(B, L, V, dt, window, seed=B * 13 + L)
+    say(f"[decode] {inp.name}")
+    m0, x0 = inp.mask.cpu().numpy(), inp.x.cpu().numpy()
+    start, end = inp.start.cpu().numpy(), inp.end.cpu().numpy()
+    ref_conf = gpu_confidence(gpu, inp)
+    for rule, p in RULES:
+        mask, x, o = _decode(gpu, inp, rule, p)
+        r = oracle.decode_step(row_source(inp.logits), B, L, m0, start, end, x0, rule, p)
+        nf, nfm = compare_selection(o["commit"].cpu().numpy(), o["n_commit"].cpu().numpy(),
+                                    r.commit, r.n_commit, r.flagged, range(B))
+        ok = ~r.flagged
+        assert np.array_equal(x.cpu().numpy()[ok], r.x[ok])
+        assert np.array_equal(mask.cpu().numpy()[ok], r.mask[ok])
+        # bitwise the same per-position outputs as fdllm_confidence
+        for name, t in zip(("tokens", "conf", "eps", "lse"), ref_conf):
+            assert torch.equal(o[name].view(torch.int32), t.view(torch.int32)), name
+        # and the same commits as fdllm_select_* fed those outputs, then reveal
+        c2 = torch.zeros((B, L), dtype=torch.uint8, device="cuda")
+        n2 = torch.zeros((B,), dtype=torch.int32, device="cuda")
+        gpu.select(rule, ref_conf[1], ref_conf[2], inp.mask, inp.start, inp.end, p, c2, n2)
+        m2, x2 = inp.mask.clone(), inp.x.clone()
+        gpu.fdllm_reveal(c2, ref_conf[0], x2, m2)
+        torch.cuda.synchronize()
+        assert torch.equal(c2, o["commit"]) and torch.equal(n2, o["n_commit"])
+        assert torch.equal(m2, mask) and torch.equal(x2, x)
+        # outputs are optional
+        mask3, x3, o3 = _decode(gpu, inp, rule, p, with_outputs=False)
+        assert torch.equal(mask3, mask) and torch.equal(x3, x) and torch.equal(o3["commit"], o["commit"])
+        say(f"  {rule}({p}): commits {int(o['n_commit'].clamp(min=0).sum())}, flagged {nf} (matching {nfm})")
+
+
+def test_crafted_profiles_on_gpu(gpu):
+    """The hand-derived worked examples, fed to the GPU selectors as float32."""
+    import test_oracle_select as ts
+    cases = ts.load_golden()
+    B, L = len(cases), 16
+    conf = torch.zeros((B, L)); eps = torch.ones((B, L))
+    mask = torch.zeros((B, L), dtype=torch.uint8)
+    for b, cs in enumerate(cases):
+        for c, pos in zip(cs["c"], cs["pos"]):
+            conf[b, pos % L] = float(c)
+            eps[b, pos % L] = float(1 - c)
+            mask[b, pos % L] = 1
+    start = torch.zeros(B, dtype=torch.int32); end = torch.full((B,), L, dtype=torch.int32)
+    args = [t.cuda() for t in (conf, eps, mask, start, end)]
+    for b, cs in enumerate(cases):
+        commit = torch.zeros((B, L), dtype=torch.uint8, device="cuda")
+        n = torch.zeros((B,), dtype=torch.int32, device="cuda")
+        gpu.select(cs["rule"], *args[:2], *args[2:], cs["param"], commit, n)
+        torch.cuda.synchronize()
+        got = sorted(np.nonzero(commit[b].cpu().numpy())[0].tolist())
+        assert int(n[b]) == cs["n_star"], cs
+        assert got == sorted(p % L for p in cs["committed"]), cs
+
+
+def test_invalid_bounds_on_device(gpu):
+    V = 64
+    for (BB, LL) in [(6, 20), (130, 100)]:
+        case = workloads.random_case(BB, LL, V, torch.bfloat16, device="cuda", seed=7, poison=False)
+        s = torch.zeros(BB, dtype=torch.int32); e = torch.zeros(BB, dtype=torch.int32)
+        for b in range(BB):
+            s[b], e[b] = [(0, LL), (5, 4), (-1, 3), (0, LL + 1), (3, 3), (10, 10 + 65)][b % 6]
+        case.start.copy_(s); case.end.copy_(e)
+        say(f"[bounds] B={BB} L={LL}")
+        mask, x, o = _decode(gpu, case, "profile", 1.0)
+        n = o["n_commit"].cpu().numpy()
+        for b in range(BB):
+            bad = b % 6 in (1, 2, 3, 5) or (b % 6 == 0 and LL > 64)
+            if bad:
+                assert n[b] == -1
+                assert not o["commit"][b].any()
+                assert torch.equal(mask[b], case.mask[b]) and torch.equal(x[b], case.x[b])
+                assert (o["tokens"][b] == -1).all()
+            elif b % 6 == 4:
+                assert n[b] == 0
+
+
+def test_determinism_and_identical_rows(gpu):
+    B, L, V = 140, 16, 126464
+    g = torch.Generator(device="cuda").manual_seed(5)
+    one = torch.randn((1, 1, V), generator=g, device="cuda") * 2
+    one[0, 0, 123] += 15.0
+    logits = one.expand(B, L, V).to(torch.bfloat16).contiguous()
+    mask = torch.ones((B, L), dtype=torch.uint8, device="cuda")
+    start = torch.zeros(B, dtype=torch.int32, device="cuda")
+    end = torch.full((B,), L, dtype=torch.int32, device="cuda")
+    x = torch.full((B, L), -1, dtype=torch.int32, device="cuda")
+    inp = workloads.StepInputs(logits, mask, start, end, x, "identical")
+    say("[determinism] fused plan, identical rows")
+    a = gpu_confidence(gpu, inp)
+    b_ = gpu_confidence(gpu, inp)
+    for t1, t2 in zip(a, b_):
+        assert torch.equal(t1.view(torch.int32), t2.view(torch.int32))
+        flat = t1.view(torch.int32).flatten()
+        assert (flat == flat[0]).all()                 # identical rows -> identical bits
+    for f in (0.5, 0.75, 1.0, 2.0):
+        _, _, op = _decode(gpu, inp, "profile", f)
+        _, _, of = _decode(gpu, inp, "factor", f)
+        assert torch.equal(op["commit"], of["commit"]) and torch.equal(op["n_commit"], of["n_commit"])
