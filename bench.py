@@ -82,6 +82,8 @@ def main():
     ap.add_argument("--cpu-blocks", type=int, default=40, help="blocks in the oracle sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-selector-sweep", action="store_true")
+    ap.add_argument("--copy-calibration-mb", type=int, default=1024,
+                    help="size of a plain device copy timed (and counted by rocprofv3) for reference")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py measures one GPU only; --gpus {args.gpus} is not supported "
@@ -98,7 +100,7 @@ def main():
     dev = torch.device("cuda", 0)
     torch.cuda.set_device(dev)
     print(f"[bench] generating config5 inputs on {torch.cuda.get_device_name(dev)}", file=sys.stderr, flush=True)
-    inp = workloads.config5(device=dev)
+    inp = workloads.config5(device=dev, progress=lambda m: print(f"[bench] {m}", file=sys.stderr, flush=True))
     B, L, V = inp.logits.shape
     positions = int(inp.mask.sum())
     logits_bytes = positions * V * inp.logits.element_size()
@@ -111,6 +113,26 @@ def main():
                 commit=torch.empty((B, L), dtype=torch.uint8, device=dev),
                 n_commit=torch.empty((B,), dtype=torch.int32, device=dev))
     torch.cuda.synchronize()
+
+    copy_ref = None
+    if args.copy_calibration_mb > 0:
+        n = args.copy_calibration_mb << 20
+        # an elementwise kernel that reads n bytes and writes n bytes: its
+        # FETCH_SIZE / WRITE_SIZE counters calibrate the fused kernel's
+        src = torch.empty(n, dtype=torch.uint8, device=dev).fill_(1)
+        dst = torch.empty_like(src)
+        torch.add(src, 1, out=dst)
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        e0.record()
+        for _ in range(5):
+            torch.add(src, 1, out=dst)
+        e1.record()
+        torch.cuda.synchronize()
+        t = e0.elapsed_time(e1) * 1e-3 / 5
+        copy_ref = {"bytes_read": n, "bytes_written": n, "seconds": t,
+                    "read_plus_write_GBps": 2 * n / t / 1e9}
+        del src, dst
 
     def run(selector, p, steps, warmup, label):
         evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
@@ -176,6 +198,7 @@ def main():
                      "kernel": "k_fused (one launch per step)",
                      "algorithmic_bytes_per_launch": algo_bytes},
         "selectors": sweep,
+        "copy_reference": copy_ref,
         "source_sha256_16": source_digest(),
     }
     if not args.no_cpu_baseline:

@@ -21,6 +21,8 @@ HIPCC_FLAGS = [
     "-shared",
     # packed-FP32 VALU forms stay disabled on this target
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+    # logits are finite by contract: max/min need no NaN quieting
+    "-fno-honor-nans", "-mno-amdgpu-ieee",
     "-Wno-unused-command-line-argument",
 ]
 

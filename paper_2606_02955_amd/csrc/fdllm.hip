@@ -41,6 +41,21 @@
 
 #include "fdllm.h"
 
+// Tile parameters (compile-time): vectors per lane per batch, and waves per
+// workgroup of the fused kernel.
+#ifndef FDLLM_FUSED_WAVES
+#define FDLLM_FUSED_WAVES 8
+#endif
+#ifndef FDLLM_U_BF16
+#define FDLLM_U_BF16 4
+#endif
+#ifndef FDLLM_U_F32
+#define FDLLM_U_F32 4
+#endif
+#ifndef FDLLM_WAVES_PER_EU
+#define FDLLM_WAVES_PER_EU 0   // minimum waves per SIMD the fused kernel is compiled for (0: no hint)
+#endif
+
 namespace fdllm {
 
 constexpr int kWave = 64;
@@ -154,6 +169,7 @@ typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 
 struct VecBf16x8 {
   static constexpr int kElems = 8;
+  static constexpr int kU = FDLLM_U_BF16;   // vectors per lane per batch
   using Raw = u32x4;
   __device__ static Raw pad() { return Raw{0xFF80FF80u, 0xFF80FF80u, 0xFF80FF80u, 0xFF80FF80u}; }
   __device__ static void unpack(const Raw& r, float (&x)[kElems]) {
@@ -165,6 +181,7 @@ struct VecBf16x8 {
 };
 struct VecF32x4 {
   static constexpr int kElems = 4;
+  static constexpr int kU = FDLLM_U_F32;
   using Raw = u32x4;
   __device__ static Raw pad() { return Raw{0xFF800000u, 0xFF800000u, 0xFF800000u, 0xFF800000u}; }
   __device__ static void unpack(const Raw& r, float (&x)[kElems]) {
@@ -174,12 +191,14 @@ struct VecF32x4 {
 };
 struct VecBf16x1 {
   static constexpr int kElems = 1;
+  static constexpr int kU = 8;
   using Raw = unsigned short;
   __device__ static Raw pad() { return (unsigned short)0xFF80u; }
   __device__ static void unpack(const Raw& r, float (&x)[kElems]) { x[0] = __uint_as_float((unsigned)r << 16); }
 };
 struct VecF32x1 {
   static constexpr int kElems = 1;
+  static constexpr int kU = 8;
   using Raw = unsigned int;
   __device__ static Raw pad() { return 0xFF800000u; }
   __device__ static void unpack(const Raw& r, float (&x)[kElems]) { x[0] = __uint_as_float(r); }
@@ -205,7 +224,7 @@ constexpr int kAcc = 4;   // independent double accumulators per lane
 // The wave handles wave-loads k = w, w+S, w+2S, ... of the row (a wave-load
 // is 64 consecutive vectors); lane l reads vector k*64 + l.
 template <class Vec, int U, int S>
-__device__ WavePartial row_pass(const typename Vec::Raw* __restrict__ row, int nvec, int w) {
+__device__ __forceinline__ WavePartial row_pass(const typename Vec::Raw* __restrict__ row, int nvec, int w) {
   using Raw = typename Vec::Raw;
   constexpr int E = Vec::kElems;
   const int lane = lane_id();
@@ -247,22 +266,48 @@ __device__ WavePartial row_pass(const typename Vec::Raw* __restrict__ row, int n
       for (int e = 0; e < E; ++e) acc[(u * E + e) % kAcc] += (double)term(x[u][e], K);
   };
 
-  int j0 = 0;
-  for (; j0 + U <= njf; j0 += U) {
-    Raw r[U];
+  // Batches of U wave-loads; the first nbf are whole (no lane past the row
+  // end).  In the steady state the loads of batch jb+1 are issued before
+  // batch jb is consumed, unconditionally, so each wave keeps a batch of
+  // 16-byte loads in flight while it computes.  The last, partial batch is
+  // loaded with per-lane predicates after the pipeline drains.
+  const int nb = (nj + U - 1) / U;
+  const int nbf = njf / U;
+  auto load_full = [&](Raw (&r)[U], int jb) {
 #pragma unroll
-    for (int u = 0; u < U; ++u) r[u] = load_stream(p + (j0 + u) * kStride);
-    consume(r, j0 / U);
-  }
-  for (; j0 < nj; j0 += U) {
-    Raw r[U];
+    for (int u = 0; u < U; ++u) r[u] = load_stream(p + (jb * U + u) * kStride);
+  };
+  auto load_part = [&](Raw (&r)[U], int jb) {
 #pragma unroll
     for (int u = 0; u < U; ++u) {
-      const int j = j0 + u;
+      const int j = jb * U + u;
       const int v = (w + j * S) * kWave + lane;
       r[u] = (j < nj && v < nvec) ? load_stream(p + j * kStride) : Vec::pad();
     }
-    consume(r, j0 / U);
+  };
+  Raw ra[U], rb[U];
+  int jb = 0;
+  if (nbf > 0) {
+    load_full(ra, 0);
+    for (; jb + 2 < nbf; jb += 2) {
+      load_full(rb, jb + 1);
+      consume(ra, jb);
+      load_full(ra, jb + 2);
+      consume(rb, jb + 1);
+    }
+    if (jb + 1 < nbf) {
+      load_full(rb, jb + 1);
+      consume(ra, jb);
+      consume(rb, jb + 1);
+      jb += 2;
+    } else {
+      consume(ra, jb);
+      jb += 1;
+    }
+  }
+  for (; jb < nb; ++jb) {
+    load_part(ra, jb);
+    consume(ra, jb);
   }
 
   // combine the lane accumulators (fixed order)
@@ -574,6 +619,9 @@ __global__ void __launch_bounds__(256) k_select(SelectIO io, int B, int L, float
 // ---------------------------------------------------------------------------
 template <class Vec, int U, int W, int R>
 __global__ void __launch_bounds__(W * kWave)
+#if FDLLM_WAVES_PER_EU > 0
+__attribute__((amdgpu_waves_per_eu(FDLLM_WAVES_PER_EU)))
+#endif
 k_fused(const typename Vec::Raw* __restrict__ logits, int B, int L, int nvec,
         uint8_t* __restrict__ mask, const int32_t* __restrict__ bstart,
         const int32_t* __restrict__ bend, int32_t* __restrict__ x, float param, RowOut out,
@@ -659,7 +707,7 @@ struct Plan {
 };
 
 constexpr int kFusedMinB = 128;
-constexpr int kFusedWaves = 8;
+constexpr int kFusedWaves = FDLLM_FUSED_WAVES;   // waves per workgroup in the fused kernel
 constexpr int kTargetWaves = 2048;   // 8 per CU on 256 CUs
 
 static Plan make_plan(int B, int L, int V, fdllm_dtype dt) {
@@ -692,7 +740,7 @@ static hipError_t launch_confidence_t(const void* logits, int B, int L, int nvec
   case SPLIT: {                                                                                 \
     using Sh = SplitShape<SPLIT>;                                                               \
     const long long grid = (nslots + Sh::kRows - 1) / Sh::kRows;                                \
-    hipLaunchKernelGGL((k_confidence<Vec, 8, SPLIT>), dim3((unsigned)grid), dim3(Sh::kThreads), \
+    hipLaunchKernelGGL((k_confidence<Vec, Vec::kU, SPLIT>), dim3((unsigned)grid), dim3(Sh::kThreads), \
                        0, st, lg, B, L, nvec, mask, bs, be, out);                               \
     break;                                                                                      \
   }
@@ -743,7 +791,7 @@ template <class Vec, int R>
 static void launch_fused_t(const void* logits, int B, int L, int nvec, uint8_t* mask,
                            const int32_t* bs, const int32_t* be, int32_t* x, float param,
                            RowOut out, uint8_t* commit, int32_t* n_commit, hipStream_t st) {
-  hipLaunchKernelGGL((k_fused<Vec, 8, kFusedWaves, R>), dim3((unsigned)B), dim3(kFusedWaves * kWave),
+  hipLaunchKernelGGL((k_fused<Vec, Vec::kU, kFusedWaves, R>), dim3((unsigned)B), dim3(kFusedWaves * kWave),
                      0, st, (const typename Vec::Raw*)logits, B, L, nvec, mask, bs, be, x, param,
                      out, commit, n_commit);
 }

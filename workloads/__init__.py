@@ -291,9 +291,11 @@ def config3(device="cpu", V: int = V_LLADA, B: int = 64, G: int = 512, blk: int 
 # background; 10% of positions carry a planted pair with gap U(0,1e-3).
 # ---------------------------------------------------------------------------
 def config5(device="cpu", V: int = V_LLADA, B: int = 1024, L: int = 32,
-            chunk: int = 32) -> StepInputs:
+            chunk: int = 32, progress: Optional[Callable[[str], None]] = None) -> StepInputs:
     logits = torch.empty((B, L, V), dtype=torch.bfloat16, device=device)
     for b0 in range(0, B, chunk):
+        if progress is not None and b0 % 256 == 0:
+            progress(f"config5 inputs: sequences {b0}..{min(B, b0 + 256) - 1}")
         for b in range(b0, min(B, b0 + chunk)):
             g = _gen(5, 0, b, device)
             rows = _gumbel(g, (L, V), device)
