@@ -3,8 +3,8 @@
  * (gfx950).  Implements one decoding step of Frechet profile decoding
  * (arXiv 2606.02955, Alg. 1): per masked position of the active block the
  * greedy token and its softmax confidence, per block the commit set chosen by
- * the Frechet profile rule (or the factor / threshold baselines), and the
- * reveal of the chosen tokens.
+ * the Frechet profile rule (its calibration-robust variant, or the factor /
+ * threshold baselines), and the reveal of the chosen tokens.
  *
  * Conventions shared by every entry point
  * ---------------------------------------
@@ -63,9 +63,10 @@ typedef struct ihipStream_t* fdllm_stream;
 typedef enum { FDLLM_BF16 = 0, FDLLM_F32 = 1 } fdllm_dtype;
 
 typedef enum {
-  FDLLM_SEL_THRESHOLD = 0, /* commit every c >= tau, else the single highest      */
-  FDLLM_SEL_FACTOR = 1,    /* largest n with (n+1)(1 - c_(n)) < f                 */
-  FDLLM_SEL_PROFILE = 2    /* largest n with G_n > 1 - f (Frechet profile rule)   */
+  FDLLM_SEL_THRESHOLD = 0, /* commit every c >= tau, else the single highest        */
+  FDLLM_SEL_FACTOR = 1,    /* largest n with (n+1)(1 - c_(n)) < f                   */
+  FDLLM_SEL_PROFILE = 2,   /* largest n with G_n > 1 - f (Frechet profile rule)     */
+  FDLLM_SEL_ROBUST = 3     /* profile rule on c_low = max(0, c - eta) (robust rule) */
 } fdllm_selector;
 
 typedef int fdllm_status;
@@ -137,6 +138,24 @@ fdllm_status fdllm_select_threshold(const float* conf, const float* eps, const u
                                     fdllm_stream stream);
 
 /*
+ * Calibration-robust Frechet profile rule (appendix "Calibration-Robust
+ * Frechet Certificates"): each reported confidence c_i is replaced by the
+ * conservative lower confidence c_low_i = max{0, c_i - eta_i}, where eta_i
+ * >= 0 is a calibration allowance (negative values count as 0), and the
+ * profile rule above is applied to the c_low profile (sorted by c_low,
+ * ties to the lower position).  With uniform eta and no clipping the score
+ * drops by exactly (n+1) eta (the calibration-penalty corollary).  The
+ * paper states the robust certificate for a set; the selector takes the
+ * largest certified prefix of the c_low order, as the plain rule does.
+ *   eta [B,L] float (in, may be NULL: then every eta_i = eta_uniform);
+ *   other arguments as for fdllm_select_profile.  eta_uniform must not be NaN.
+ */
+fdllm_status fdllm_select_robust(const float* conf, const float* eps, const float* eta,
+                                 float eta_uniform, const uint8_t* mask, const int32_t* block_start,
+                                 const int32_t* block_end, int B, int L, float f, uint8_t* commit,
+                                 int32_t* n_commit, fdllm_stream stream);
+
+/*
  * Reveal (Alg. 1, reveal step): for every (b,i) with commit[b,i] != 0 set
  * x[b,i] = tokens[b,i] and mask[b,i] = 0.  Other entries are untouched.
  *   commit [B,L] uint8 (in); tokens [B,L] int32 (in); x [B,L] int32 (in/out);
@@ -150,6 +169,8 @@ fdllm_status fdllm_reveal(const uint8_t* commit, const int32_t* tokens, int32_t*
  * fdllm_confidence, then the selector `sel` with `param` (f, or tau for the
  * threshold rule), then the reveal, fused.  Large batches run as one kernel
  * (one workgroup per sequence); small batches as two kernels.
+ *   eta, eta_uniform: calibration allowance of FDLLM_SEL_ROBUST (as in
+ *   fdllm_select_robust); ignored by the other selectors.
  *   mask [B,L] uint8 (in/out: committed positions are cleared);
  *   x    [B,L] int32 (in/out: committed positions receive their token);
  *   tokens, conf, eps, lse [B,L], commit [B,L], n_commit [B]: optional
@@ -160,10 +181,10 @@ fdllm_status fdllm_reveal(const uint8_t* commit, const int32_t* tokens, int32_t*
  */
 fdllm_status fdllm_decode_step(const void* logits, fdllm_dtype dtype, int B, int L, int V,
                                uint8_t* mask, const int32_t* block_start, const int32_t* block_end,
-                               int32_t* x, fdllm_selector sel, float param, int32_t* tokens,
-                               float* conf, float* eps, float* lse, uint8_t* commit,
-                               int32_t* n_commit, void* workspace, size_t workspace_bytes,
-                               fdllm_stream stream);
+                               int32_t* x, fdllm_selector sel, float param, const float* eta,
+                               float eta_uniform, int32_t* tokens, float* conf, float* eps,
+                               float* lse, uint8_t* commit, int32_t* n_commit, void* workspace,
+                               size_t workspace_bytes, fdllm_stream stream);
 
 /* Workspace bytes fdllm_decode_step needs for these sizes (0 = none). */
 fdllm_status fdllm_workspace_size(int B, int L, int V, fdllm_dtype dtype, size_t* bytes);

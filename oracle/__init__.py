@@ -7,9 +7,10 @@ CPU restatement of what one decoding step of the paper's method computes:
     confidence, the complement 1 - c and the log-sum-exp of the logits
     (Sec. 3 "Notation"; Alg. 1, the per-position loop);
   * per block, the commit set chosen by the Frechet profile rule (Sec. 3,
-    "Frechet profile quantities"; Alg. 1 selection), by Fast-dLLM's factor rule
-    and by the threshold rule (Sec. 2, "Confidence-Aware Parallel Decoding";
-    Sec. 5, "Baselines");
+    "Frechet profile quantities"; Alg. 1 selection), by its calibration-robust
+    variant (appendix "Calibration-Robust Frechet Certificates"), by
+    Fast-dLLM's factor rule and by the threshold rule (Sec. 2,
+    "Confidence-Aware Parallel Decoding"; Sec. 5, "Baselines");
   * the reveal of the chosen tokens (Alg. 1, reveal step).
 
 It shares no code with the HIP library and imports nothing from it.  Only the
@@ -29,11 +30,11 @@ propositions; see the docstrings for which passage each one follows.
 from .confidence import position_confidence, confidence
 from .rules import (sorted_order, factor_n_star, profile_n_star, profile_literal_n_star,
                      profile_adaptive_n_star, threshold_set, select_block, select, SelectResult,
-                     frechet_quantities, FLAG_WINDOW)
+                     frechet_quantities, robust_eps, FLAG_WINDOW)
 from .step import decode_step, StepResult
 
 __all__ = [
     "position_confidence", "confidence", "sorted_order", "factor_n_star", "profile_n_star",
     "profile_literal_n_star", "profile_adaptive_n_star", "threshold_set", "select_block",
-    "select", "SelectResult", "frechet_quantities", "FLAG_WINDOW", "decode_step", "StepResult",
+    "select", "SelectResult", "frechet_quantities", "robust_eps", "FLAG_WINDOW", "decode_step", "StepResult",
 ]

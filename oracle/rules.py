@@ -28,7 +28,14 @@ Rules (n runs over 1..m):
     adaptive-factor form is used, which keeps the equal-confidence reduction
     exact for every f;
   * threshold (Sec. 2 "Confidence-Aware Parallel Decoding"): commit every
-    candidate with c_i >= tau.
+    candidate with c_i >= tau;
+  * calibration-robust profile (appendix "Calibration-Robust Frechet
+    Certificates"): the Frechet profile rule on the conservative lower
+    confidences c_low_i = max{0, c^_i - eta_i}, sorted by c_low.  The paper
+    states the robust certificate L_eta(S) > U_eta(S) for a set S; for a
+    fixed size the top-|S| set by c_low maximises both sum c_low and
+    min c_low, so the selector takes the largest prefix of the c_low order
+    whose robust score exceeds delta (the same reading as the plain rule).
 
 n* is the largest accepted n; when no n is accepted one candidate is still
 committed (Sec. 3 "with the convention n* = 1 ... ensuring progress"; for the
@@ -47,7 +54,7 @@ from __future__ import annotations
 
 import dataclasses
 from fractions import Fraction as Q
-from typing import List, Sequence
+from typing import List, Optional, Sequence
 
 import numpy as np
 
@@ -55,12 +62,23 @@ FLAG_WINDOW = 1e-6
 
 
 def _q(v) -> Q:
-    return Q(float(v))
+    return v if isinstance(v, Q) else Q(float(v))
 
 
 def sorted_order(eps: Sequence[float], positions: Sequence[int]) -> List[int]:
     """Candidate indices by confidence descending (eps ascending), ties by position."""
-    return sorted(range(len(eps)), key=lambda k: (float(eps[k]), int(positions[k])))
+    return sorted(range(len(eps)), key=lambda k: (_q(eps[k]), int(positions[k])))
+
+
+def robust_eps(eps: Sequence[float], eta: Sequence[float]) -> List[Q]:
+    """1 - c_low for the calibration-robust rule, exactly.
+
+    Appendix "Calibration-Robust Frechet Certificates": the reported
+    confidence c^_i is replaced by the conservative lower confidence
+    c_low_i = max{0, c^_i - eta_i}, i.e. eps_low_i = min{1, eps^_i + eta_i}.
+    The allowance eta_i is >= 0 in the paper; a negative value is taken as 0.
+    """
+    return [min(Q(1), _q(e) + max(Q(0), _q(h))) for e, h in zip(eps, eta)]
 
 
 def frechet_quantities(eps_sorted: Sequence[float]):
@@ -154,13 +172,20 @@ class SelectResult:
 
 
 def select_block(eps: Sequence[float], conf: Sequence[float], positions: Sequence[int],
-                 rule: str, param: float, window: float = FLAG_WINDOW) -> SelectResult:
-    """Commit set of one block's candidates under `rule` in {profile, factor, threshold}."""
+                 rule: str, param: float, window: float = FLAG_WINDOW,
+                 eta: Optional[Sequence[float]] = None) -> SelectResult:
+    """Commit set of one block's candidates under `rule`.
+
+    rule is one of profile, factor, threshold, robust; `eta` (per candidate)
+    is the calibration allowance of the robust rule.
+    """
     m = len(eps)
     if m == 0:
         return SelectResult(0, [], False, [], [])
+    if rule == "robust":
+        eps = robust_eps(eps, eta if eta is not None else [0.0] * m)
     order = sorted_order(eps, positions)
-    eps_s = [float(eps[k]) for k in order]
+    eps_s = [_q(eps[k]) for k in order]
     reasons: List[str] = []
     wq = _q(window)
     if rule == "threshold":
@@ -177,7 +202,7 @@ def select_block(eps: Sequence[float], conf: Sequence[float], positions: Sequenc
     if rule == "factor":
         n_star = factor_n_star(eps_s, param)
         lhs = factor_lhs(eps_s)
-    elif rule == "profile":
+    elif rule in ("profile", "robust"):
         n_star = profile_n_star(eps_s, param)
         lhs = profile_lhs(eps_s)
     else:
@@ -195,15 +220,17 @@ def select_block(eps: Sequence[float], conf: Sequence[float], positions: Sequenc
     return SelectResult(n_star, committed, bool(reasons), reasons, order)
 
 
-def select(eps, conf, mask, start, end, rule: str, param: float):
+def select(eps, conf, mask, start, end, rule: str, param: float, eta=None):
     """Selection for a batch of blocks given per-position eps/conf arrays [B, L].
 
     Candidates of sequence b: masked positions in [start[b], end[b]).
+    `eta` ([B, L] array or scalar) is the robust rule's calibration allowance.
     Returns (commit [B,L] uint8, n_commit [B] int64, flagged [B] bool, results).
     """
     eps = np.asarray(eps)
     conf = np.asarray(conf)
     mask = np.asarray(mask)
+    eta_arr = None if eta is None else np.broadcast_to(np.asarray(eta, dtype=np.float64), mask.shape)
     B, L = mask.shape
     commit = np.zeros((B, L), dtype=np.uint8)
     n_commit = np.zeros((B,), dtype=np.int64)
@@ -214,7 +241,8 @@ def select(eps, conf, mask, start, end, rule: str, param: float):
         if not (0 <= lo <= hi <= L):
             raise ValueError(f"bad block bounds for sequence {b}: [{lo},{hi}) with L={L}")
         pos = [i for i in range(lo, hi) if mask[b, i]]
-        r = select_block([eps[b, i] for i in pos], [conf[b, i] for i in pos], pos, rule, param)
+        r = select_block([eps[b, i] for i in pos], [conf[b, i] for i in pos], pos, rule, param,
+                         eta=None if eta_arr is None else [eta_arr[b, i] for i in pos])
         for i in r.committed:
             commit[b, i] = 1
         n_commit[b] = r.n_commit

@@ -29,17 +29,19 @@ class StepResult:
     details: list
 
 
-def decode_step(logits, B: int, L: int, mask, start, end, x, rule: str, param: float) -> StepResult:
+def decode_step(logits, B: int, L: int, mask, start, end, x, rule: str, param: float,
+                eta=None) -> StepResult:
     """Oracle decode step.
 
     ``logits`` is a [B][L] indexable of 1-D rows or a callable row(b, i);
     only candidate rows are read.  ``mask``/``x`` are [B, L] arrays and are
-    not modified; the updated copies are returned.
+    not modified; the updated copies are returned.  ``eta`` is the robust
+    rule's calibration allowance ([B, L] or scalar).
     """
     mask = np.array(mask, dtype=np.uint8, copy=True)
     x = np.array(x, dtype=np.int64, copy=True)
     tokens, conf, eps, lse = confidence(logits, B, L, mask, start, end)
-    commit, n_commit, flagged, details = select(eps, conf, mask, start, end, rule, param)
+    commit, n_commit, flagged, details = select(eps, conf, mask, start, end, rule, param, eta=eta)
     hit = commit.astype(bool)
     x[hit] = tokens[hit]
     mask[hit] = 0

@@ -18,15 +18,16 @@ _PKG = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_PKG, "libfdllm.so")
 
 BF16, F32 = 0, 1
-SEL_THRESHOLD, SEL_FACTOR, SEL_PROFILE = 0, 1, 2
-SELECTORS = {"threshold": SEL_THRESHOLD, "factor": SEL_FACTOR, "profile": SEL_PROFILE}
+SEL_THRESHOLD, SEL_FACTOR, SEL_PROFILE, SEL_ROBUST = 0, 1, 2, 3
+SELECTORS = {"threshold": SEL_THRESHOLD, "factor": SEL_FACTOR, "profile": SEL_PROFILE,
+             "robust": SEL_ROBUST}
 MAX_BLOCK = 64
 
 OK = 0
 ERR_INVALID_ARG, ERR_UNSUPPORTED_DTYPE, ERR_SIZE, ERR_WORKSPACE, ERR_HIP = -1, -2, -3, -4, -5
 
 EXPORTS = ("fdllm_confidence", "fdllm_select_profile", "fdllm_select_factor",
-           "fdllm_select_threshold", "fdllm_reveal", "fdllm_decode_step",
+           "fdllm_select_threshold", "fdllm_select_robust", "fdllm_reveal", "fdllm_decode_step",
            "fdllm_workspace_size", "fdllm_status_string")
 
 _lib = None
@@ -53,8 +54,10 @@ def load(path: Optional[str] = None) -> ctypes.CDLL:
     for name in ("fdllm_select_profile", "fdllm_select_factor", "fdllm_select_threshold"):
         getattr(lib, name).argtypes = [vp, vp, vp, vp, vp, i32, i32, f32, vp, vp, vp]
         getattr(lib, name).restype = i32
+    lib.fdllm_select_robust.argtypes = [vp, vp, vp, f32, vp, vp, vp, i32, i32, f32, vp, vp, vp]
+    lib.fdllm_select_robust.restype = i32
     lib.fdllm_reveal.argtypes = [vp, vp, vp, vp, i32, i32, vp]
-    lib.fdllm_decode_step.argtypes = [vp, i32, i32, i32, i32, vp, vp, vp, vp, i32, f32,
+    lib.fdllm_decode_step.argtypes = [vp, i32, i32, i32, i32, vp, vp, vp, vp, i32, f32, vp, f32,
                                       vp, vp, vp, vp, vp, vp, vp, sz, vp]
     lib.fdllm_workspace_size.argtypes = [i32, i32, i32, i32, ctypes.POINTER(sz)]
     lib.fdllm_status_string.argtypes = [i32]
@@ -138,6 +141,20 @@ def fdllm_select_threshold(conf, eps, mask, block_start, block_end, tau, commit,
     _select("fdllm_select_threshold", conf, eps, mask, block_start, block_end, tau, commit, n_commit)
 
 
+def fdllm_select_robust(conf, eps, mask, block_start, block_end, f, commit, n_commit=None,
+                        eta=None, eta_uniform: float = 0.0):
+    """Calibration-robust profile rule; eta [B,L] or a uniform allowance (see fdllm.h)."""
+    B, L = conf.shape
+    st = load().fdllm_select_robust(
+        _ptr(conf, torch.float32, (B, L), "conf"), _ptr(eps, torch.float32, (B, L), "eps"),
+        _ptr(eta, torch.float32, (B, L), "eta"), float(eta_uniform),
+        _ptr(mask, torch.uint8, (B, L), "mask"), _ptr(block_start, torch.int32, (B,), "block_start"),
+        _ptr(block_end, torch.int32, (B,), "block_end"), B, L, float(f),
+        _ptr(commit, torch.uint8, (B, L), "commit"), _ptr(n_commit, torch.int32, (B,), "n_commit"),
+        _stream(conf.device))
+    _check(st, "fdllm_select_robust")
+
+
 def fdllm_reveal(commit, tokens, x, mask):
     B, L = commit.shape
     st = load().fdllm_reveal(
@@ -156,7 +173,7 @@ def fdllm_workspace_size(B: int, L: int, V: int, dtype: torch.dtype) -> int:
 
 def fdllm_decode_step(logits, mask, block_start, block_end, x, selector: str, param: float,
                       tokens=None, conf=None, eps=None, lse=None, commit=None, n_commit=None,
-                      workspace: Optional[torch.Tensor] = None):
+                      workspace: Optional[torch.Tensor] = None, eta=None, eta_uniform: float = 0.0):
     """One fused decoding step; mask and x are updated in place (see fdllm.h)."""
     B, L, V = logits.shape
     if selector not in SELECTORS:
@@ -172,7 +189,7 @@ def fdllm_decode_step(logits, mask, block_start, block_end, x, selector: str, pa
         _ptr(logits, name="logits"), _dtype_code(logits), B, L, V,
         _ptr(mask, torch.uint8, (B, L), "mask"), _ptr(block_start, torch.int32, (B,), "block_start"),
         _ptr(block_end, torch.int32, (B,), "block_end"), _ptr(x, torch.int32, (B, L), "x"),
-        SELECTORS[selector], float(param),
+        SELECTORS[selector], float(param), _ptr(eta, torch.float32, (B, L), "eta"), float(eta_uniform),
         _ptr(tokens, torch.int32, (B, L), "tokens"), _ptr(conf, torch.float32, (B, L), "conf"),
         _ptr(eps, torch.float32, (B, L), "eps"), _ptr(lse, torch.float32, (B, L), "lse"),
         _ptr(commit, torch.uint8, (B, L), "commit"), _ptr(n_commit, torch.int32, (B,), "n_commit"),
@@ -181,7 +198,13 @@ def fdllm_decode_step(logits, mask, block_start, block_end, x, selector: str, pa
     return workspace
 
 
-def select(selector: str, conf, eps, mask, block_start, block_end, param, commit, n_commit=None):
+def select(selector: str, conf, eps, mask, block_start, block_end, param, commit, n_commit=None,
+           eta=None, eta_uniform: float = 0.0):
+    """Dispatch to fdllm_select_<selector>."""
+    if selector == "robust":
+        fdllm_select_robust(conf, eps, mask, block_start, block_end, param, commit, n_commit,
+                            eta=eta, eta_uniform=eta_uniform)
+        return
     {"profile": fdllm_select_profile, "factor": fdllm_select_factor,
      "threshold": fdllm_select_threshold}[selector](conf, eps, mask, block_start, block_end,
                                                     param, commit, n_commit)

@@ -22,7 +22,7 @@ HIPCC_FLAGS = [
     # packed-FP32 VALU forms stay disabled on this target
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
     # logits are finite by contract: max/min need no NaN quieting
-    "-fno-honor-nans", "-mno-amdgpu-ieee",
+    "-Xarch_device", "-fno-honor-nans", "-Xarch_device", "-mno-amdgpu-ieee",
     "-Wno-unused-command-line-argument",
 ]
 

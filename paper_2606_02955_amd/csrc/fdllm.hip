@@ -31,9 +31,10 @@
 //     v_readlane; partials of a split row meet in LDS in fixed order, so
 //     results do not depend on scheduling.
 // The selection runs in one wavefront per block: a 64-lane bitonic sort of
-// (eps bits, slot) keys, a double-precision prefix scan of the heterogeneity
+// (eps, slot) keys, a double-precision prefix scan of the heterogeneity
 // bonus, a ballot for n*, and ds_permute to route each decision back to its
-// position.
+// position.  The calibration-robust rule (the appendix on calibration-robust
+// certificates) is the profile rule on eps_low = min(1, eps + eta).
 #include <hip/hip_runtime.h>
 
 #include <math.h>
@@ -508,19 +509,21 @@ __device__ __forceinline__ double wave_scan_f64(double v, int lane) {
 }
 
 // Decides the commit set of one block.  Lane j describes slot j of the block
-// (position start + j): `valid` marks a candidate, `key` orders candidates by
-// confidence descending (smaller key = more confident), `e` is the candidate's
-// eps = 1 - c in double and `conf` its confidence (threshold rule only).
-// Returns n* (the number of commits) and sets `commit_slot` for lane j's slot.
+// (position start + j): `valid` marks a candidate, `e` is its complement
+// eps = 1 - c in double (the order is by e ascending, i.e. confidence
+// descending, ties to the lower position) and `conf` its confidence (used by
+// the threshold rule only).  Returns n* (the number of commits) and sets
+// `commit_slot` for lane j's own slot.
 template <int R>
-__device__ int select_wave(bool valid, unsigned key, double e, float conf, float param,
-                           bool& commit_slot) {
+__device__ int select_wave(bool valid, double e, float conf, float param, bool& commit_slot) {
   const int lane = lane_id();
   const unsigned long long vmask = __ballot(valid);
   const int m = __popcll(vmask);
-  // [invalid:1][key:32][slot:6]: candidates first, by key, ties by position
+  // key [invalid:1][bits(e) >> 5 : 57][slot:6]; e in [0, 1] has bits < 2^62,
+  // and dropping 5 mantissa bits keeps float32-derived values exact
+  const unsigned long long eb = (unsigned long long)__double_as_longlong(e);
   const unsigned long long k64 = ((unsigned long long)(valid ? 0u : 1u) << 63) |
-                                 ((unsigned long long)key << 6) | (unsigned)lane;
+                                 ((eb >> 5) << 6) | (unsigned)lane;
   const unsigned long long sk = wave_sort(k64, lane);
   const int rank_slot = (int)(sk & 63u);   // slot held by sorted rank `lane`
   const bool rvalid = lane < m;
@@ -556,17 +559,19 @@ __device__ int select_wave(bool valid, unsigned key, double e, float conf, float
   return nstar;
 }
 
-// Sort key and eps of a candidate from float eps (preferred) or conf only.
-__device__ __forceinline__ void cand_key(const float* eps_arr, float c, size_t idx, unsigned& key,
-                                         double& e) {
-  if (eps_arr) {
-    const float ev = eps_arr[idx];
-    key = __float_as_uint(ev);          // eps >= 0: bit order is value order
-    e = (double)ev;
-  } else {
-    key = ~__float_as_uint(c);          // c >= 0: descending c = ascending ~bits
-    e = 1.0 - (double)c;                // exact in double
-  }
+// eps of a candidate from float eps (preferred) or conf only, then the
+// calibration allowance of the robust rule: eps_low = min(1, eps + max(0, eta)).
+struct EtaIn {
+  const float* eta;      // [B, L] per-position allowance, or null
+  float uniform;         // allowance when eta is null
+};
+
+__device__ __forceinline__ double cand_eps(const float* eps_arr, float c, size_t idx) {
+  return eps_arr ? (double)eps_arr[idx] : 1.0 - (double)c;   // 1 - c is exact in double
+}
+__device__ __forceinline__ double robust_eps(double e, const EtaIn& eta, size_t idx) {
+  const float h = eta.eta ? eta.eta[idx] : eta.uniform;
+  return fmin(1.0, e + fmax((double)h, 0.0));
 }
 
 struct SelectIO {
@@ -579,9 +584,10 @@ struct SelectIO {
   int32_t* n_commit;          // may be null
   const int32_t* tokens;      // reveal source (may be null: no reveal)
   int32_t* x;                 // reveal target (may be null: no reveal)
+  EtaIn eta;                  // calibration allowance (robust rule)
 };
 
-template <int R>
+template <int R, bool Robust>
 __global__ void __launch_bounds__(256) k_select(SelectIO io, int B, int L, float param) {
   const int lane = threadIdx.x % kWave;
   const int b = blockIdx.x * 4 + threadIdx.x / kWave;
@@ -593,14 +599,14 @@ __global__ void __launch_bounds__(256) k_select(SelectIO io, int B, int L, float
   const bool inwin = ok && lane < e_end - s;
   const bool valid = inwin && io.mask[row + i] != 0;
   float c = 0.0f;
-  unsigned key = 0xFFFFFFFFu;
   double e = 1.0;
   if (valid) {
     c = io.conf[row + i];
-    cand_key(io.eps, c, row + i, key, e);
+    e = cand_eps(io.eps, c, row + i);
+    if constexpr (Robust) e = robust_eps(e, io.eta, row + i);
   }
   bool take = false;
-  const int nstar = select_wave<R>(valid, key, e, c, param, take);
+  const int nstar = select_wave<R>(valid, e, c, param, take);
   if (io.commit) {
     // every entry of row b written once: window slots by their lane, the rest zero
     for (int q = lane; q < L; q += kWave)
@@ -617,15 +623,15 @@ __global__ void __launch_bounds__(256) k_select(SelectIO io, int B, int L, float
 // ---------------------------------------------------------------------------
 // kernel: fused decode step, one workgroup of W waves per sequence
 // ---------------------------------------------------------------------------
-template <class Vec, int U, int W, int R>
+template <class Vec, int U, int W, int R, bool Robust>
 __global__ void __launch_bounds__(W * kWave)
 #if FDLLM_WAVES_PER_EU > 0
 __attribute__((amdgpu_waves_per_eu(FDLLM_WAVES_PER_EU)))
 #endif
 k_fused(const typename Vec::Raw* __restrict__ logits, int B, int L, int nvec,
         uint8_t* __restrict__ mask, const int32_t* __restrict__ bstart,
-        const int32_t* __restrict__ bend, int32_t* __restrict__ x, float param, RowOut out,
-        uint8_t* __restrict__ commit, int32_t* __restrict__ n_commit) {
+        const int32_t* __restrict__ bend, int32_t* __restrict__ x, float param, EtaIn eta,
+        RowOut out, uint8_t* __restrict__ commit, int32_t* __restrict__ n_commit) {
   __shared__ int s_cand[kMaxBlock];       // candidate slots, compacted
   __shared__ int s_tok[kMaxBlock];
   __shared__ float s_conf[kMaxBlock];
@@ -670,10 +676,12 @@ k_fused(const typename Vec::Raw* __restrict__ logits, int B, int L, int nvec,
   __syncthreads();
   if (wave != 0) return;
   const bool valid = lane < len && mask[row0 + s + lane] != 0;
-  const float ev = valid ? s_eps[lane] : 1.0f;
+  double ev = valid ? (double)s_eps[lane] : 1.0;
+  if constexpr (Robust) {
+    if (valid) ev = robust_eps(ev, eta, row0 + s + lane);
+  }
   bool take = false;
-  const int nstar = select_wave<R>(valid, __float_as_uint(ev), (double)ev,
-                                   valid ? s_conf[lane] : 0.0f, param, take);
+  const int nstar = select_wave<R>(valid, ev, valid ? s_conf[lane] : 0.0f, param, take);
   if (valid) {
     if (commit) commit[row0 + s + lane] = take ? 1 : 0;
     if (take) {
@@ -775,41 +783,52 @@ static hipError_t launch_select(fdllm_selector sel, const SelectIO& io, int B, i
   const dim3 grid((unsigned)((B + 3) / 4)), block(256);
   switch (sel) {
     case FDLLM_SEL_THRESHOLD:
-      hipLaunchKernelGGL(k_select<kThreshold>, grid, block, 0, st, io, B, L, param);
+      hipLaunchKernelGGL((k_select<kThreshold, false>), grid, block, 0, st, io, B, L, param);
       break;
     case FDLLM_SEL_FACTOR:
-      hipLaunchKernelGGL(k_select<kFactor>, grid, block, 0, st, io, B, L, param);
+      hipLaunchKernelGGL((k_select<kFactor, false>), grid, block, 0, st, io, B, L, param);
+      break;
+    case FDLLM_SEL_ROBUST:
+      hipLaunchKernelGGL((k_select<kProfile, true>), grid, block, 0, st, io, B, L, param);
       break;
     default:
-      hipLaunchKernelGGL(k_select<kProfile>, grid, block, 0, st, io, B, L, param);
+      hipLaunchKernelGGL((k_select<kProfile, false>), grid, block, 0, st, io, B, L, param);
       break;
   }
   return hipGetLastError();
 }
 
-template <class Vec, int R>
+template <class Vec, int R, bool Robust>
 static void launch_fused_t(const void* logits, int B, int L, int nvec, uint8_t* mask,
                            const int32_t* bs, const int32_t* be, int32_t* x, float param,
-                           RowOut out, uint8_t* commit, int32_t* n_commit, hipStream_t st) {
-  hipLaunchKernelGGL((k_fused<Vec, Vec::kU, kFusedWaves, R>), dim3((unsigned)B), dim3(kFusedWaves * kWave),
-                     0, st, (const typename Vec::Raw*)logits, B, L, nvec, mask, bs, be, x, param,
-                     out, commit, n_commit);
+                           EtaIn eta, RowOut out, uint8_t* commit, int32_t* n_commit,
+                           hipStream_t st) {
+  hipLaunchKernelGGL((k_fused<Vec, Vec::kU, kFusedWaves, R, Robust>), dim3((unsigned)B),
+                     dim3(kFusedWaves * kWave), 0, st, (const typename Vec::Raw*)logits, B, L, nvec,
+                     mask, bs, be, x, param, eta, out, commit, n_commit);
 }
 
 template <class Vec>
 static hipError_t launch_fused_v(fdllm_selector sel, const void* logits, int B, int L, int nvec,
                                  uint8_t* mask, const int32_t* bs, const int32_t* be, int32_t* x,
-                                 float param, RowOut out, uint8_t* commit, int32_t* n_commit,
-                                 hipStream_t st) {
+                                 float param, EtaIn eta, RowOut out, uint8_t* commit,
+                                 int32_t* n_commit, hipStream_t st) {
   switch (sel) {
     case FDLLM_SEL_THRESHOLD:
-      launch_fused_t<Vec, kThreshold>(logits, B, L, nvec, mask, bs, be, x, param, out, commit, n_commit, st);
+      launch_fused_t<Vec, kThreshold, false>(logits, B, L, nvec, mask, bs, be, x, param, eta, out,
+                                             commit, n_commit, st);
       break;
     case FDLLM_SEL_FACTOR:
-      launch_fused_t<Vec, kFactor>(logits, B, L, nvec, mask, bs, be, x, param, out, commit, n_commit, st);
+      launch_fused_t<Vec, kFactor, false>(logits, B, L, nvec, mask, bs, be, x, param, eta, out,
+                                          commit, n_commit, st);
+      break;
+    case FDLLM_SEL_ROBUST:
+      launch_fused_t<Vec, kProfile, true>(logits, B, L, nvec, mask, bs, be, x, param, eta, out,
+                                          commit, n_commit, st);
       break;
     default:
-      launch_fused_t<Vec, kProfile>(logits, B, L, nvec, mask, bs, be, x, param, out, commit, n_commit, st);
+      launch_fused_t<Vec, kProfile, false>(logits, B, L, nvec, mask, bs, be, x, param, eta, out,
+                                           commit, n_commit, st);
       break;
   }
   return hipGetLastError();
@@ -817,16 +836,20 @@ static hipError_t launch_fused_v(fdllm_selector sel, const void* logits, int B, 
 
 static hipError_t launch_fused(fdllm_selector sel, const void* logits, fdllm_dtype dt, int B, int L,
                                int V, uint8_t* mask, const int32_t* bs, const int32_t* be,
-                               int32_t* x, float param, RowOut out, uint8_t* commit,
+                               int32_t* x, float param, EtaIn eta, RowOut out, uint8_t* commit,
                                int32_t* n_commit, hipStream_t st) {
   if (vec_path(logits, V, dt)) {
     if (dt == FDLLM_BF16)
-      return launch_fused_v<VecBf16x8>(sel, logits, B, L, V / 8, mask, bs, be, x, param, out, commit, n_commit, st);
-    return launch_fused_v<VecF32x4>(sel, logits, B, L, V / 4, mask, bs, be, x, param, out, commit, n_commit, st);
+      return launch_fused_v<VecBf16x8>(sel, logits, B, L, V / 8, mask, bs, be, x, param, eta, out,
+                                       commit, n_commit, st);
+    return launch_fused_v<VecF32x4>(sel, logits, B, L, V / 4, mask, bs, be, x, param, eta, out,
+                                    commit, n_commit, st);
   }
   if (dt == FDLLM_BF16)
-    return launch_fused_v<VecBf16x1>(sel, logits, B, L, V, mask, bs, be, x, param, out, commit, n_commit, st);
-  return launch_fused_v<VecF32x1>(sel, logits, B, L, V, mask, bs, be, x, param, out, commit, n_commit, st);
+    return launch_fused_v<VecBf16x1>(sel, logits, B, L, V, mask, bs, be, x, param, eta, out, commit,
+                                     n_commit, st);
+  return launch_fused_v<VecF32x1>(sel, logits, B, L, V, mask, bs, be, x, param, eta, out, commit,
+                                  n_commit, st);
 }
 
 static bool sizes_ok(int B, int L, int V) {
@@ -889,11 +912,11 @@ fdllm_status fdllm_confidence(const void* logits, fdllm_dtype dtype, int B, int 
 static fdllm_status select_common(fdllm_selector sel, const float* conf, const float* eps,
                                   const uint8_t* mask, const int32_t* bs, const int32_t* be, int B,
                                   int L, float param, uint8_t* commit, int32_t* n_commit,
-                                  fdllm_stream stream) {
+                                  fdllm_stream stream, EtaIn eta = EtaIn{nullptr, 0.0f}) {
   if (B < 0 || L < 1) return FDLLM_ERR_INVALID_ARG;
   if (B == 0) return FDLLM_OK;
   if (!conf || !mask || !bs || !be || !commit) return FDLLM_ERR_INVALID_ARG;
-  SelectIO io{conf, eps, const_cast<uint8_t*>(mask), bs, be, commit, n_commit, nullptr, nullptr};
+  SelectIO io{conf, eps, const_cast<uint8_t*>(mask), bs, be, commit, n_commit, nullptr, nullptr, eta};
   hipError_t err = launch_select(sel, io, B, L, param, (hipStream_t)stream);
   return err == hipSuccess ? FDLLM_OK : FDLLM_ERR_HIP;
 }
@@ -922,6 +945,15 @@ fdllm_status fdllm_select_threshold(const float* conf, const float* eps, const u
                        commit, n_commit, stream);
 }
 
+fdllm_status fdllm_select_robust(const float* conf, const float* eps, const float* eta,
+                                 float eta_uniform, const uint8_t* mask, const int32_t* block_start,
+                                 const int32_t* block_end, int B, int L, float f, uint8_t* commit,
+                                 int32_t* n_commit, fdllm_stream stream) {
+  if (!(eta_uniform == eta_uniform)) return FDLLM_ERR_INVALID_ARG;   // NaN
+  return select_common(FDLLM_SEL_ROBUST, conf, eps, mask, block_start, block_end, B, L, f, commit,
+                       n_commit, stream, EtaIn{eta, eta_uniform});
+}
+
 fdllm_status fdllm_reveal(const uint8_t* commit, const int32_t* tokens, int32_t* x, uint8_t* mask,
                           int B, int L, fdllm_stream stream) {
   if (B < 0 || L < 1) return FDLLM_ERR_INVALID_ARG;
@@ -937,13 +969,15 @@ fdllm_status fdllm_reveal(const uint8_t* commit, const int32_t* tokens, int32_t*
 
 fdllm_status fdllm_decode_step(const void* logits, fdllm_dtype dtype, int B, int L, int V,
                                uint8_t* mask, const int32_t* block_start, const int32_t* block_end,
-                               int32_t* x, fdllm_selector sel, float param, int32_t* tokens,
-                               float* conf, float* eps, float* lse, uint8_t* commit,
-                               int32_t* n_commit, void* workspace, size_t workspace_bytes,
-                               fdllm_stream stream) {
+                               int32_t* x, fdllm_selector sel, float param, const float* eta,
+                               float eta_uniform, int32_t* tokens, float* conf, float* eps,
+                               float* lse, uint8_t* commit, int32_t* n_commit, void* workspace,
+                               size_t workspace_bytes, fdllm_stream stream) {
   if (dtype != FDLLM_BF16 && dtype != FDLLM_F32) return FDLLM_ERR_UNSUPPORTED_DTYPE;
-  if (sel != FDLLM_SEL_THRESHOLD && sel != FDLLM_SEL_FACTOR && sel != FDLLM_SEL_PROFILE)
+  if (sel != FDLLM_SEL_THRESHOLD && sel != FDLLM_SEL_FACTOR && sel != FDLLM_SEL_PROFILE &&
+      sel != FDLLM_SEL_ROBUST)
     return FDLLM_ERR_INVALID_ARG;
+  if (!(eta_uniform == eta_uniform)) return FDLLM_ERR_INVALID_ARG;
   if (B < 0 || L < 1) return FDLLM_ERR_INVALID_ARG;
   if (!sizes_ok(B, L, V)) return FDLLM_ERR_SIZE;
   if (B == 0) return FDLLM_OK;
@@ -951,10 +985,11 @@ fdllm_status fdllm_decode_step(const void* logits, fdllm_dtype dtype, int B, int
   const Plan p = make_plan(B, L, V, dtype);
   hipStream_t st = (hipStream_t)stream;
   RowOut out{tokens, conf, eps, lse};
+  const EtaIn etain{eta, eta_uniform};
   hipError_t err;
   if (p.fused) {
-    err = launch_fused(sel, logits, dtype, B, L, V, mask, block_start, block_end, x, param, out,
-                       commit, n_commit, st);
+    err = launch_fused(sel, logits, dtype, B, L, V, mask, block_start, block_end, x, param, etain,
+                       out, commit, n_commit, st);
     return err == hipSuccess ? FDLLM_OK : FDLLM_ERR_HIP;
   }
   // two kernels: confidence into the caller's arrays or the workspace, then select+reveal
@@ -969,7 +1004,7 @@ fdllm_status fdllm_decode_step(const void* logits, fdllm_dtype dtype, int B, int
   out = RowOut{tokens, conf, eps, lse};
   err = launch_confidence(logits, dtype, B, L, V, p.split, mask, block_start, block_end, out, st);
   if (err != hipSuccess) return FDLLM_ERR_HIP;
-  SelectIO io{conf, eps, mask, block_start, block_end, commit, n_commit, tokens, x};
+  SelectIO io{conf, eps, mask, block_start, block_end, commit, n_commit, tokens, x, etain};
   err = launch_select(sel, io, B, L, param, st);
   return err == hipSuccess ? FDLLM_OK : FDLLM_ERR_HIP;
 }

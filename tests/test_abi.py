@@ -74,13 +74,21 @@ def test_error_paths_enqueue_nothing(lib):
         assert f(p, null, null, p, p, 2, 4, 1.0, p, null, null) == fd.ERR_INVALID_ARG
         assert f(p, null, p, p, p, 2, 0, 1.0, p, null, null) == fd.ERR_INVALID_ARG
         assert f(null, null, null, null, null, 0, 4, 1.0, null, null, null) == 0
+    f = lib.fdllm_select_robust
+    assert f(null, null, null, 0.0, p, p, p, 2, 4, 1.0, p, null, null) == fd.ERR_INVALID_ARG
+    assert f(p, null, null, 0.0, p, p, p, 2, 4, 1.0, null, null, null) == fd.ERR_INVALID_ARG
+    assert f(p, null, null, float("nan"), p, p, p, 2, 4, 1.0, p, null, null) == fd.ERR_INVALID_ARG
+    assert f(null, null, null, 0.1, null, null, null, 0, 4, 1.0, null, null, null) == 0
     assert lib.fdllm_reveal(null, p, p, p, 2, 4, null) == fd.ERR_INVALID_ARG
     assert lib.fdllm_reveal(p, p, p, p, -1, 4, null) == fd.ERR_INVALID_ARG
     # decode step: bad selector, dtype, null in/out arrays, missing workspace
     args = lambda **kw: [kw.get("logits", p), kw.get("dt", 0), kw.get("B", 8), 32, kw.get("V", 64),
                          kw.get("mask", p), p, p, kw.get("x", p), kw.get("sel", 2), 1.0,
+                         null, kw.get("eta_u", 0.0),
                          null, null, null, null, null, null, kw.get("ws", null), kw.get("wsb", 0), null]
-    assert lib.fdllm_decode_step(*args(sel=3)) == fd.ERR_INVALID_ARG
+    assert lib.fdllm_decode_step(*args(sel=4)) == fd.ERR_INVALID_ARG
+    assert lib.fdllm_decode_step(*args(sel=-1)) == fd.ERR_INVALID_ARG
+    assert lib.fdllm_decode_step(*args(sel=3, eta_u=float("nan"))) == fd.ERR_INVALID_ARG
     assert lib.fdllm_decode_step(*args(dt=9)) == fd.ERR_UNSUPPORTED_DTYPE
     assert lib.fdllm_decode_step(*args(logits=null)) == fd.ERR_INVALID_ARG
     assert lib.fdllm_decode_step(*args(mask=null)) == fd.ERR_INVALID_ARG

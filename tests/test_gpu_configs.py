@@ -24,7 +24,7 @@ def _free():
     torch.cuda.empty_cache()
 
 
-def _decode(gpu, inp, rule, p, mask=None, x=None):
+def _decode(gpu, inp, rule, p, mask=None, x=None, eta=None, eta_uniform=0.0):
     B, L, V = inp.logits.shape
     mask = inp.mask.clone() if mask is None else mask
     x = inp.x.clone() if x is None else x
@@ -33,7 +33,8 @@ def _decode(gpu, inp, rule, p, mask=None, x=None):
              lse=torch.empty((B, L), device="cuda"),
              commit=torch.empty((B, L), dtype=torch.uint8, device="cuda"),
              n_commit=torch.empty((B,), dtype=torch.int32, device="cuda"))
-    gpu.fdllm_decode_step(inp.logits, mask, inp.start, inp.end, x, rule, p, **o)
+    gpu.fdllm_decode_step(inp.logits, mask, inp.start, inp.end, x, rule, p, eta=eta,
+                          eta_uniform=eta_uniform, **o)
     torch.cuda.synchronize()
     return mask, x, o
 
@@ -124,12 +125,19 @@ def test_config5_sampled(gpu):
     # matched-factor dominance holds exactly in the GPU arithmetic
     for p in (1.0, 0.75):
         assert (res[("profile", p)]["n_commit"] >= res[("factor", p)]["n_commit"]).all()
+    # the calibration-robust rule never commits more than the plain rule
+    mask_r, x_r, o_r = _decode(gpu, inp, "robust", 1.0, eta_uniform=0.02)
+    assert (o_r["n_commit"] <= res[("profile", 1.0)]["n_commit"]).all()
+    assert (o_r["n_commit"] >= 1).all()
+    say(f"  robust(1.0, eta=0.02): mean commits/block {float(o_r['n_commit'].float().mean()):.3f}")
     nf, nfm, worst, r = _check_step(inp, res[("profile", 1.0)], sample, "profile", 1.0)
     say(f"  oracle on {len(sample)} blocks: flagged={nf} worst={worst}")
-    for rule, p in [("factor", 1.0), ("threshold", 0.9), ("profile", 0.75)]:
+    res[("robust", 1.0)] = o_r
+    for rule, p in [("factor", 1.0), ("threshold", 0.9), ("profile", 0.75), ("robust", 1.0)]:
         oc, on, fl, _ = oracle.select(r.eps, r.conf, np.where(np.isin(np.arange(B), sample)[:, None],
                                       inp.mask.cpu().numpy(), 0), inp.start.cpu().numpy(),
-                                      inp.end.cpu().numpy(), rule, p)
+                                      inp.end.cpu().numpy(), rule, p,
+                                      eta=0.02 if rule == "robust" else None)
         o = res[(rule, p)]
         nf, nfm = compare_selection(o["commit"].cpu().numpy(), o["n_commit"].cpu().numpy(), oc, on, fl, sample)
         say(f"  {rule}({p}) on sample: flagged={nf}")

@@ -16,7 +16,23 @@ from parity import (say, row_source, candidates, compare_rows, gpu_confidence,
 pytestmark = pytest.mark.gpu
 
 RULES = [("profile", 1.0), ("profile", 0.75), ("profile", 2.0), ("factor", 1.0),
-         ("factor", 0.75), ("threshold", 0.9)]
+         ("factor", 0.75), ("threshold", 0.9), ("robust", 1.0), ("robust", 0.75)]
+
+
+def _eta(rule, B, L, seed):
+    """(eta tensor or None, uniform value, oracle eta) for a rule: per-position
+    allowances for robust(1.0), a uniform one for robust(0.75)."""
+    if rule != "robust":
+        return None, 0.0, None
+    g = torch.Generator(device="cuda").manual_seed(seed)
+    eta = torch.rand((B, L), generator=g, device="cuda") * 0.1
+    return eta, 0.0, eta.double().cpu().numpy()
+
+
+def _eta_for(rule, p, B, L, seed):
+    if rule == "robust" and p == 0.75:
+        return None, 0.03, 0.03
+    return _eta(rule, B, L, seed)
 
 SMALL = [
     # (B, L, V, dtype, window)  -- vector and scalar paths, ragged wave-loads
@@ -61,16 +77,18 @@ def test_select_vs_oracle_on_gpu_confidences(gpu, B, L, V, dt, window):
         e_in = eps if use_eps else None
         e_or = eps.double().cpu().numpy() if use_eps else 1.0 - conf.double().cpu().numpy()
         for rule, p in RULES:
+            eta, eta_u, eta_o = _eta_for(rule, p, B, L, B + L)
             commit = torch.full((B, L), 9, dtype=torch.uint8, device="cuda")
             n = torch.full((B,), -9, dtype=torch.int32, device="cuda")
-            gpu.select(rule, conf, e_in, inp.mask, inp.start, inp.end, p, commit, n)
+            gpu.select(rule, conf, e_in, inp.mask, inp.start, inp.end, p, commit, n, eta=eta, eta_uniform=eta_u)
             torch.cuda.synchronize()
-            oc, on, flagged, _ = oracle.select(e_or, conf.double().cpu().numpy(), mask, start, end, rule, p)
+            oc, on, flagged, _ = oracle.select(e_or, conf.double().cpu().numpy(), mask, start, end, rule, p,
+                                               eta=eta_o)
             nf, nfm = compare_selection(commit.cpu().numpy(), n.cpu().numpy(), oc, on, flagged, range(B))
             say(f"  {rule}({p}) eps={'gpu' if use_eps else '1-conf'}: flagged {nf} (matching {nfm})")
 
 
-def _decode(gpu, inp, rule, p, with_outputs=True):
+def _decode(gpu, inp, rule, p, with_outputs=True, eta=None, eta_uniform=0.0):
     B, L, V = inp.logits.shape
     d = "cuda"
     mask, x = inp.mask.clone(), inp.x.clone()
@@ -81,7 +99,8 @@ def _decode(gpu, inp, rule, p, with_outputs=True):
                 n_commit=torch.full((B,), -9, dtype=torch.int32, device=d))
     if not with_outputs:
         outs = dict(commit=outs["commit"], n_commit=outs["n_commit"])
-    gpu.fdllm_decode_step(inp.logits, mask, inp.start, inp.end, x, rule, p, **outs)
+    gpu.fdllm_decode_step(inp.logits, mask, inp.start, inp.end, x, rule, p, eta=eta,
+                          eta_uniform=eta_uniform, **outs)
     torch.cuda.synchronize()
     return mask, x, outs
 
@@ -94,8 +113,9 @@ def test_decode_step_vs_oracle(gpu, B, L, V, dt, window):
     start, end = inp.start.cpu().numpy(), inp.end.cpu().numpy()
     ref_conf = gpu_confidence(gpu, inp)
     for rule, p in RULES:
-        mask, x, o = _decode(gpu, inp, rule, p)
-        r = oracle.decode_step(row_source(inp.logits), B, L, m0, start, end, x0, rule, p)
+        eta, eta_u, eta_o = _eta_for(rule, p, B, L, B * 3 + L)
+        mask, x, o = _decode(gpu, inp, rule, p, eta=eta, eta_uniform=eta_u)
+        r = oracle.decode_step(row_source(inp.logits), B, L, m0, start, end, x0, rule, p, eta=eta_o)
         nf, nfm = compare_selection(o["commit"].cpu().numpy(), o["n_commit"].cpu().numpy(),
                                     r.commit, r.n_commit, r.flagged, range(B))
         ok = ~r.flagged
@@ -107,14 +127,15 @@ def test_decode_step_vs_oracle(gpu, B, L, V, dt, window):
         # and the same commits as fdllm_select_* fed those outputs, then reveal
         c2 = torch.zeros((B, L), dtype=torch.uint8, device="cuda")
         n2 = torch.zeros((B,), dtype=torch.int32, device="cuda")
-        gpu.select(rule, ref_conf[1], ref_conf[2], inp.mask, inp.start, inp.end, p, c2, n2)
+        gpu.select(rule, ref_conf[1], ref_conf[2], inp.mask, inp.start, inp.end, p, c2, n2,
+                   eta=eta, eta_uniform=eta_u)
         m2, x2 = inp.mask.clone(), inp.x.clone()
         gpu.fdllm_reveal(c2, ref_conf[0], x2, m2)
         torch.cuda.synchronize()
         assert torch.equal(c2, o["commit"]) and torch.equal(n2, o["n_commit"])
         assert torch.equal(m2, mask) and torch.equal(x2, x)
         # outputs are optional
-        mask3, x3, o3 = _decode(gpu, inp, rule, p, with_outputs=False)
+        mask3, x3, o3 = _decode(gpu, inp, rule, p, with_outputs=False, eta=eta, eta_uniform=eta_u)
         assert torch.equal(mask3, mask) and torch.equal(x3, x) and torch.equal(o3["commit"], o["commit"])
         say(f"  {rule}({p}): commits {int(o['n_commit'].clamp(min=0).sum())}, flagged {nf} (matching {nfm})")
 
@@ -124,19 +145,22 @@ def test_crafted_profiles_on_gpu(gpu):
     import test_oracle_select as ts
     cases = ts.load_golden()
     B, L = len(cases), 16
-    conf = torch.zeros((B, L)); eps = torch.ones((B, L))
+    conf = torch.zeros((B, L)); eps = torch.ones((B, L)); eta = torch.zeros((B, L))
     mask = torch.zeros((B, L), dtype=torch.uint8)
     for b, cs in enumerate(cases):
-        for c, pos in zip(cs["c"], cs["pos"]):
+        for k, (c, pos) in enumerate(zip(cs["c"], cs["pos"])):
             conf[b, pos % L] = float(c)
             eps[b, pos % L] = float(1 - c)
             mask[b, pos % L] = 1
+            if cs["eta"] is not None:
+                eta[b, pos % L] = cs["eta"][k]
     start = torch.zeros(B, dtype=torch.int32); end = torch.full((B,), L, dtype=torch.int32)
     args = [t.cuda() for t in (conf, eps, mask, start, end)]
+    eta = eta.cuda()
     for b, cs in enumerate(cases):
         commit = torch.zeros((B, L), dtype=torch.uint8, device="cuda")
         n = torch.zeros((B,), dtype=torch.int32, device="cuda")
-        gpu.select(cs["rule"], *args[:2], *args[2:], cs["param"], commit, n)
+        gpu.select(cs["rule"], *args[:2], *args[2:], cs["param"], commit, n, eta=eta)
         torch.cuda.synchronize()
         got = sorted(np.nonzero(commit[b].cpu().numpy())[0].tolist())
         assert int(n[b]) == cs["n_star"], cs

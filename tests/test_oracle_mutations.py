@@ -86,6 +86,12 @@ SELECT_MUTANTS = {
                                   or ([order[0]] if len(order) else []))),
     # no progress fallback
     "no_fallback": ("_fallback", lambda m: 0),
+    # robust rule: allowance added to the confidence instead of subtracted
+    "robust_sign": ("robust_eps",
+        lambda eps, eta: [max(Q(0), Q(float(e)) - Q(float(h))) for e, h in zip(eps, eta)]),
+    # robust rule: lower confidence not clipped at zero
+    "robust_no_clip": ("robust_eps",
+        lambda eps, eta: [Q(float(e)) + Q(float(h)) for e, h in zip(eps, eta)]),
 }
 
 
@@ -111,7 +117,7 @@ def test_select_mutants_are_caught(kind, monkeypatch):
     name, fn = SELECT_MUTANTS[kind]
     monkeypatch.setattr(rules, name, fn)
     caught = 0
-    for chk in [ts.run_golden, ts.check_subset_bruteforce]:
+    for chk in [ts.run_golden, ts.check_subset_bruteforce, ts.check_robust_rule]:
         try:
             chk()
         except AssertionError:

@@ -27,27 +27,29 @@ def load_golden():
         if not line or line.startswith("#"):
             continue
         rule, param, confs, n_star, committed, flagged, note = [p.strip() for p in line.split("|")]
-        if ";" in confs:
-            confs, pos = confs.split(";")
-            pos = [int(v) for v in pos.strip()[len("pos="):].split(",")]
-        else:
-            pos = None
-        c = [Q(v) for v in confs.strip().split(",")]
-        if pos is None:
-            pos = list(range(len(c)))
+        parts = [q.strip() for q in confs.split(";")]
+        c = [Q(v) for v in parts[0].split(",")]
+        pos, eta = list(range(len(c))), None
+        for extra in parts[1:]:
+            key, val = extra.split("=")
+            vals = val.split(",")
+            if key == "pos":
+                pos = [int(v) for v in vals]
+            elif key == "eta":
+                eta = [float(v) for v in vals] * (len(c) if len(vals) == 1 else 1)
         cases.append(dict(rule=rule, param=float(param), c=c, pos=pos, n_star=int(n_star),
                           committed=[int(v) for v in committed.split(",")],
-                          flagged=bool(int(flagged)), note=note))
+                          flagged=bool(int(flagged)), note=note, eta=eta))
     return cases
 
 
 def run_golden(select_block=oracle.select_block):
     cases = load_golden()
-    assert len(cases) >= 20
+    assert len(cases) >= 25
     for cs in cases:
         eps = [float(1 - c) for c in cs["c"]]
         conf = [float(c) for c in cs["c"]]
-        r = select_block(eps, conf, cs["pos"], cs["rule"], cs["param"])
+        r = select_block(eps, conf, cs["pos"], cs["rule"], cs["param"], eta=cs["eta"])
         assert r.n_commit == cs["n_star"], cs
         assert r.committed == sorted(cs["committed"]), cs
         assert r.flagged == cs["flagged"], (cs, r.reasons)
@@ -286,3 +288,81 @@ def test_batch_select_matches_blocks():
             assert n_commit[b] == r.n_commit
             assert sorted(np.nonzero(commit[b])[0].tolist()) == r.committed
             assert set(r.committed) <= set(pos)
+
+
+def check_robust_rule(select_block=oracle.select_block, frechet_quantities=oracle.frechet_quantities):
+    """Calibration-robust rule: eta = 0 is the profile rule; the calibration
+    penalty G^(eta)_n = G^_n - (n+1) eta holds exactly where its assumptions
+    hold; commits never grow with a larger uniform eta."""
+    rng = np.random.default_rng(41)
+    pen = 0
+    for eps in random_profiles(rng, 400, quantise=None) + random_profiles(rng, 200, quantise=64):
+        m = len(eps)
+        pos = list(range(m))
+        conf = [1 - e for e in eps]
+        for f in (0.5, 0.75, 1.0, 2.0):
+            a = select_block(eps, conf, pos, "profile", f)
+            b = select_block(eps, conf, pos, "robust", f, eta=[0.0] * m)
+            assert (a.n_commit, a.committed) == (b.n_commit, b.committed)
+            prev = m + 1
+            for eta in (0.0, 0.01, 0.05, 0.2, 0.6):
+                r = select_block(eps, conf, pos, "robust", f, eta=[eta] * m)
+                assert r.n_commit <= prev
+                prev = r.n_commit
+        eta = float(rng.choice([0.01, 0.03, 0.1]))
+        plain = frechet_quantities(eps)
+        rob = frechet_quantities(oracle.robust_eps(eps, [eta] * m))
+        c = [1 - Q(e) for e in eps]
+        for qp, qr in zip(plain, rob):
+            n = qp["n"]
+            no_clip = all(c[j] >= Q(eta) for j in range(n))
+            if no_clip and qr["sum_c"] - (n - 1) > 0:
+                pen += 1
+                assert qr["G"] == qp["G"] - (n + 1) * Q(eta)
+    assert pen > 300
+
+
+def check_robust_subsets_and_certificate(select_block=oracle.select_block,
+                                         frechet_quantities=oracle.frechet_quantities):
+    rng = np.random.default_rng(43)
+    for trial in range(150):
+        m = int(rng.integers(1, 8))
+        c = [Q(int(v), 64) for v in rng.integers(1, 65, m)]
+        eta = [Q(int(v), 64) for v in rng.integers(0, 9, m)]
+        low = [max(Q(0), ci - hi) for ci, hi in zip(c, eta)]
+        positions = list(range(m))
+        for f in (0.25, 0.75, 1.0):
+            best, sets = subset_brute_force(low, positions, "profile", f)
+            r = select_block([float(1 - v) for v in c], [float(v) for v in c], positions, "robust", f,
+                             eta=[float(h) for h in eta])
+            if best == 0:
+                top = max(range(m), key=lambda k: (low[k], -positions[k]))
+                assert r.n_commit == 1 and r.committed == [positions[top]]
+            else:
+                assert r.n_commit == best and r.committed in sets
+    # robust certificate on tiny joints: any envelope c_low <= true marginal
+    certified = 0
+    for trial in range(500):
+        n = int(rng.integers(1, 4))
+        V = int(rng.integers(2, 5))
+        P = _random_joint(rng, n, V, rng.choice([0.0, 0.8, 0.95]))
+        marg = [P.sum(axis=tuple(a for a in range(n) if a != j)) for j in range(n)]
+        xs = tuple(int(np.argmax(mj)) for mj in marg)
+        r_true = [float(marg[j][xs[j]]) for j in range(n)]
+        eta = rng.uniform(0, 0.05, n)
+        c_low = [max(0.0, r - h) for r, h in zip(r_true, eta)]
+        q = frechet_quantities(sorted(1.0 - v for v in c_low))[-1]
+        if q["L"] > q["U"]:
+            certified += 1
+            flat = P.ravel()
+            top = np.argsort(flat)[::-1]
+            assert np.unravel_index(top[0], P.shape) == xs and flat[top[0]] > flat[top[1]]
+    assert certified > 50
+
+
+def test_robust_rule():
+    check_robust_rule()
+
+
+def test_robust_subsets_and_certificate():
+    check_robust_subsets_and_certificate()
