@@ -30,10 +30,11 @@
  *   masked positions of the active block).  Logits of other rows are never
  *   read; their outputs are tokens = -1, conf = 0, eps = 1, lse = 0,
  *   commit = 0.
- * Bounds.  A block needs 0 <= start <= end <= L and end - start <= 64
- *   (FDLLM_MAX_BLOCK, one 64-lane wavefront).  Bounds live in device memory
- *   and are checked on the device: a sequence with invalid bounds gets no
- *   commits, default outputs and n_commit = -1.
+ * Bounds.  A block needs 0 <= start <= end <= L and end - start <= 1024
+ *   (FDLLM_MAX_BLOCK).  Blocks of up to 64 positions are selected within one
+ *   64-lane wavefront, larger ones (block-size ablations) by a workgroup.
+ *   Bounds live in device memory and are checked on the device: a sequence
+ *   with invalid bounds gets no commits, default outputs and n_commit = -1.
  * Logits.  Must be finite with |logit| < 1e30 (NaN/inf are not supported).
  * Ties.  The argmax takes the lowest vocabulary index; the confidence sort
  *   puts equal values at the lower position first.
@@ -77,7 +78,7 @@ typedef int fdllm_status;
 #define FDLLM_ERR_WORKSPACE (-4)         /* workspace missing or too small           */
 #define FDLLM_ERR_HIP (-5)               /* the HIP runtime rejected a launch        */
 
-#define FDLLM_MAX_BLOCK 64
+#define FDLLM_MAX_BLOCK 1024
 
 /*
  * Greedy token, confidence, complement and log-sum-exp of every candidate

@@ -81,12 +81,13 @@ def robust_eps(eps: Sequence[float], eta: Sequence[float]) -> List[Q]:
     return [min(Q(1), _q(e) + max(Q(0), _q(h))) for e, h in zip(eps, eta)]
 
 
-def frechet_quantities(eps_sorted: Sequence[float]):
+def frechet_quantities(eps_sorted: Sequence[float], with_bonus: bool = True):
     """Exact L_n, U_n, G_n, F_n, B_n for n = 1..m of a sorted profile.
 
     Sec. 3 (L_n, U_n, G_n) and the heterogeneity-bonus proposition
     (F_n = (n+1) c_(n) - n, B_n = sum_{j<n} (c_(j) - c_(n))), with
-    c_(j) = 1 - eps_(j).  Returns a list of dicts of Fractions.
+    c_(j) = 1 - eps_(j).  Returns a list of dicts of Fractions.  B_n is summed
+    term by term (quadratic in m); with_bonus=False leaves it out (None).
     """
     c = [1 - _q(e) for e in eps_sorted]
     out = []
@@ -96,7 +97,7 @@ def frechet_quantities(eps_sorted: Sequence[float]):
         L = max(Q(0), running - (n - 1))
         U = 1 - c[n - 1]
         F = (n + 1) * c[n - 1] - n
-        B = sum((c[j] - c[n - 1] for j in range(n - 1)), Q(0))
+        B = sum((c[j] - c[n - 1] for j in range(n - 1)), Q(0)) if with_bonus else None
         out.append(dict(n=n, L=L, U=U, G=L - U, F=F, B=B, sum_c=running))
     return out
 
@@ -132,7 +133,7 @@ def factor_n_star(eps_sorted: Sequence[float], f: float) -> int:
 def profile_literal_n_star(eps_sorted: Sequence[float], f: float) -> int:
     """n* = max{n : L_n - U_n > delta}, delta = 1 - f, literal clipped L_n."""
     delta = 1 - _q(f)
-    acc = [q["n"] for q in frechet_quantities(eps_sorted) if q["G"] > delta]
+    acc = [q["n"] for q in frechet_quantities(eps_sorted, with_bonus=False) if q["G"] > delta]
     return max(acc) if acc else _fallback(len(eps_sorted))
 
 

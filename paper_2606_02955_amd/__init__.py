@@ -21,7 +21,7 @@ BF16, F32 = 0, 1
 SEL_THRESHOLD, SEL_FACTOR, SEL_PROFILE, SEL_ROBUST = 0, 1, 2, 3
 SELECTORS = {"threshold": SEL_THRESHOLD, "factor": SEL_FACTOR, "profile": SEL_PROFILE,
              "robust": SEL_ROBUST}
-MAX_BLOCK = 64
+MAX_BLOCK = 1024
 
 OK = 0
 ERR_INVALID_ARG, ERR_UNSUPPORTED_DTYPE, ERR_SIZE, ERR_WORKSPACE, ERR_HIP = -1, -2, -3, -4, -5

@@ -60,7 +60,8 @@
 namespace fdllm {
 
 constexpr int kWave = 64;
-constexpr int kMaxBlock = FDLLM_MAX_BLOCK;
+constexpr int kMaxBlock = FDLLM_MAX_BLOCK;   // largest active block (workgroup selection)
+constexpr int kWaveBlock = kWave;            // blocks up to this size select in one wavefront
 constexpr float kLog2e = 1.44269504088896340736f;
 constexpr float kNegInf = -__builtin_huge_valf();
 constexpr float kRefFloor = -3.0e38f;   // exponent reference before any element
@@ -508,6 +509,15 @@ __device__ __forceinline__ double wave_scan_f64(double v, int lane) {
   return v;
 }
 
+// Sort key of a candidate: [invalid:1][bits(e) >> 9 : 53][slot:10].  e is in
+// [0, 1], so bits(e) < 2^62; dropping 9 of the 52 mantissa bits keeps every
+// float32-derived value exact (ties below 2^-43 relative fall to the slot).
+constexpr unsigned long long kSlotMask = 1023ull;
+__device__ __forceinline__ unsigned long long sort_key(bool valid, double e, int slot) {
+  const unsigned long long eb = (unsigned long long)__double_as_longlong(e);
+  return ((unsigned long long)(valid ? 0u : 1u) << 63) | ((eb >> 9) << 10) | (unsigned)slot;
+}
+
 // Decides the commit set of one block.  Lane j describes slot j of the block
 // (position start + j): `valid` marks a candidate, `e` is its complement
 // eps = 1 - c in double (the order is by e ascending, i.e. confidence
@@ -519,13 +529,8 @@ __device__ int select_wave(bool valid, double e, float conf, float param, bool& 
   const int lane = lane_id();
   const unsigned long long vmask = __ballot(valid);
   const int m = __popcll(vmask);
-  // key [invalid:1][bits(e) >> 5 : 57][slot:6]; e in [0, 1] has bits < 2^62,
-  // and dropping 5 mantissa bits keeps float32-derived values exact
-  const unsigned long long eb = (unsigned long long)__double_as_longlong(e);
-  const unsigned long long k64 = ((unsigned long long)(valid ? 0u : 1u) << 63) |
-                                 ((eb >> 5) << 6) | (unsigned)lane;
-  const unsigned long long sk = wave_sort(k64, lane);
-  const int rank_slot = (int)(sk & 63u);   // slot held by sorted rank `lane`
+  const unsigned long long sk = wave_sort(sort_key(valid, e, lane), lane);
+  const int rank_slot = (int)(sk & kSlotMask);   // slot held by sorted rank `lane`
   const bool rvalid = lane < m;
   bool take;
   int nstar;
@@ -574,6 +579,122 @@ __device__ __forceinline__ double robust_eps(double e, const EtaIn& eta, size_t 
   return fmin(1.0, e + fmax((double)h, 0.0));
 }
 
+// ---------------------------------------------------------------------------
+// selection of one block of up to kMaxBlock candidates by a workgroup
+// ---------------------------------------------------------------------------
+// Block-size ablations go beyond one wavefront; the same rules are evaluated
+// with the keys sorted in LDS (bitonic network over N = 2^k >= len entries)
+// and a fixed-order double-precision scan of the heterogeneity bonus.
+constexpr int kMaxWaves = 16;          // waves of the largest selecting workgroup
+struct WideLds {
+  unsigned long long key[kMaxBlock];   // sort keys by slot; after the sort, by rank
+  double e[kMaxBlock];                 // eps by slot
+  float conf[kMaxBlock];               // confidence by slot
+  int tok[kMaxBlock];                  // greedy token by slot (fused kernel)
+  int flag[kMaxBlock];                 // commit decision by slot
+  double wsum[kMaxWaves];              // per-wave totals of the scan
+  int m;                               // number of candidates
+  int nstar;
+  int count;
+};
+
+__device__ __forceinline__ int next_pow2(int v) {
+  int n = 1;
+  while (n < v) n <<= 1;
+  return n;
+}
+
+// Requires (then a barrier): key[0, N) for every slot, padding slots invalid;
+// e and conf of every candidate slot; m.  Every thread of the NT-thread
+// workgroup calls it.  Leaves flag[slot] for every slot in [0, N), returns n*.
+// The first kOwners threads own the ranks, so the rounding order of the scan
+// depends on N only, not on the workgroup size of the calling kernel.
+constexpr int kOwners = 256;
+
+template <int R, int NT>
+__device__ int select_wg(WideLds& sh, int N, float param) {
+  static_assert(NT % kWave == 0 && NT >= kOwners && NT / kWave <= kMaxWaves, "workgroup shape");
+  const int tid = threadIdx.x;
+  const int lane = tid % kWave;
+  const int wave = tid / kWave;
+  for (int k = 2; k <= N; k <<= 1) {            // bitonic sort, ascending
+    for (int j = k >> 1; j > 0; j >>= 1) {
+      for (int i = tid; i < (N >> 1); i += NT) {
+        const int a = ((i & ~(j - 1)) << 1) | (i & (j - 1));
+        const int c = a | j;
+        const unsigned long long ka = sh.key[a], kc = sh.key[c];
+        if ((ka > kc) == ((a & k) == 0)) {
+          sh.key[a] = kc;
+          sh.key[c] = ka;
+        }
+      }
+      __syncthreads();
+    }
+  }
+  const int m = sh.m;
+  if (tid == 0) {
+    sh.nstar = 0;
+    sh.count = 0;
+  }
+  // thread tid < kOwners owns the contiguous ranks [r0, r0 + kpt), the others none
+  const int kpt = tid < kOwners ? (N + kOwners - 1) / kOwners : 0;
+  const int r0 = tid * kpt;
+  int nstar;
+  if constexpr (R == kThreshold) {
+    int cnt = 0;
+    for (int q = 0; q < kpt; ++q) {
+      const int r = r0 + q;
+      if (r < m && sh.conf[(int)(sh.key[r] & kSlotMask)] >= param) ++cnt;
+    }
+    __syncthreads();
+    if (cnt) atomicAdd(&sh.count, cnt);
+    __syncthreads();
+    const int total = sh.count;
+    for (int q = 0; q < kpt && r0 + q < N; ++q) {
+      const int r = r0 + q;
+      const int slot = (int)(sh.key[r] & kSlotMask);
+      const bool take = total > 0 ? (r < m && sh.conf[slot] >= param) : (r == 0 && m > 0);
+      sh.flag[slot] = take ? 1 : 0;
+    }
+    nstar = total > 0 ? total : (m > 0 ? 1 : 0);
+  } else {
+    // t_r = r (e_(r) - e_(r-1)) for 0-based rank r >= 1; B at rank r = sum_{r' <= r} t_r'
+    double local = 0.0;
+    if constexpr (R == kProfile) {
+      for (int q = 0; q < kpt; ++q) {
+        const int r = r0 + q;
+        if (r >= 1 && r < m)
+          local += (double)r * (sh.e[(int)(sh.key[r] & kSlotMask)] -
+                                sh.e[(int)(sh.key[r - 1] & kSlotMask)]);
+      }
+    }
+    const double incl = wave_scan_f64(local, lane);
+    if (lane == kWave - 1) sh.wsum[wave] = incl;
+    __syncthreads();
+    double b = shfl_up_f64(incl, 1);
+    if (lane == 0) b = 0.0;
+    for (int w = 0; w < wave; ++w) b += sh.wsum[w];   // terms of all lower ranks
+    int best = 0;
+    for (int q = 0; q < kpt; ++q) {
+      const int r = r0 + q;
+      if (r >= m) break;
+      const double er = sh.e[(int)(sh.key[r] & kSlotMask)];
+      if constexpr (R == kProfile) {
+        if (r >= 1) b += (double)r * (er - sh.e[(int)(sh.key[r - 1] & kSlotMask)]);
+      }
+      const double lhs = (double)(r + 2) * er - (R == kProfile ? b : 0.0);
+      if (lhs < (double)param) best = r + 1;
+    }
+    if (best) atomicMax(&sh.nstar, best);
+    __syncthreads();
+    nstar = sh.nstar > 0 ? sh.nstar : (m > 0 ? 1 : 0);
+    for (int q = 0; q < kpt && r0 + q < N; ++q)
+      sh.flag[(int)(sh.key[r0 + q] & kSlotMask)] = r0 + q < nstar ? 1 : 0;
+  }
+  __syncthreads();
+  return nstar;
+}
+
 struct SelectIO {
   const float* conf;
   const float* eps;           // may be null
@@ -587,6 +708,34 @@ struct SelectIO {
   EtaIn eta;                  // calibration allowance (robust rule)
 };
 
+// One wavefront decides a block of len <= 64 slots (lane j = slot j) and
+// writes its in-window commit flags, reveal and n_commit.
+template <int R, bool Robust>
+__device__ __forceinline__ void select_block_wave(const SelectIO& io, size_t row, int b, int s,
+                                                  int len, bool ok, float param) {
+  const int lane = lane_id();
+  const bool inwin = lane < len;
+  const size_t i = row + (size_t)(s + lane);
+  const bool valid = inwin && io.mask[i] != 0;
+  float c = 0.0f;
+  double e = 1.0;
+  if (valid) {
+    c = io.conf[i];
+    e = cand_eps(io.eps, c, i);
+    if constexpr (Robust) e = robust_eps(e, io.eta, i);
+  }
+  bool take = false;
+  const int nstar = select_wave<R>(valid, e, c, param, take);
+  if (io.commit && inwin) io.commit[i] = take ? 1 : 0;
+  if (take && io.x) {
+    io.x[i] = io.tokens[i];
+    io.mask[i] = 0;
+  }
+  if (io.n_commit && lane == 0) io.n_commit[b] = ok ? nstar : -1;
+}
+
+// Rows of at most 64 positions: one wavefront per block, four blocks per
+// workgroup.
 template <int R, bool Robust>
 __global__ void __launch_bounds__(256) k_select(SelectIO io, int B, int L, float param) {
   const int lane = threadIdx.x % kWave;
@@ -595,29 +744,65 @@ __global__ void __launch_bounds__(256) k_select(SelectIO io, int B, int L, float
   const size_t row = (size_t)b * L;
   const int s = io.bstart[b], e_end = io.bend[b];
   const bool ok = window_ok(s, e_end, L);
-  const int i = s + lane;
-  const bool inwin = ok && lane < e_end - s;
-  const bool valid = inwin && io.mask[row + i] != 0;
-  float c = 0.0f;
-  double e = 1.0;
-  if (valid) {
-    c = io.conf[row + i];
-    e = cand_eps(io.eps, c, row + i);
-    if constexpr (Robust) e = robust_eps(e, io.eta, row + i);
-  }
-  bool take = false;
-  const int nstar = select_wave<R>(valid, e, c, param, take);
+  const int len = ok ? e_end - s : 0;
   if (io.commit) {
     // every entry of row b written once: window slots by their lane, the rest zero
     for (int q = lane; q < L; q += kWave)
-      if (!(ok && q >= s && q < e_end)) io.commit[row + q] = 0;
-    if (inwin) io.commit[row + i] = take ? 1 : 0;
+      if (q < s || q >= s + len) io.commit[row + q] = 0;
   }
-  if (take && io.x) {
-    io.x[row + i] = io.tokens[row + i];
-    io.mask[row + i] = 0;
+  select_block_wave<R, Robust>(io, row, b, s, len, ok, param);
+}
+
+// Rows of more than 64 positions: one workgroup per block; blocks of at most
+// 64 candidates still select in one wavefront, larger ones in the workgroup.
+template <int R, bool Robust, int NT>
+__global__ void __launch_bounds__(NT) k_select_wide(SelectIO io, int B, int L, float param) {
+  __shared__ WideLds sh;
+  const int tid = threadIdx.x;
+  const int b = blockIdx.x;
+  const size_t row = (size_t)b * L;
+  const int s = io.bstart[b], e_end = io.bend[b];
+  const bool ok = window_ok(s, e_end, L);
+  const int len = ok ? e_end - s : 0;
+  if (io.commit) {
+    for (int q = tid; q < L; q += NT)
+      if (q < s || q >= s + len) io.commit[row + q] = 0;
   }
-  if (io.n_commit && lane == 0) io.n_commit[b] = ok ? nstar : -1;
+  if (len <= kWave) {
+    if (tid < kWave) select_block_wave<R, Robust>(io, row, b, s, len, ok, param);
+    return;
+  }
+  const int N = next_pow2(len);
+  if (tid == 0) sh.m = 0;
+  __syncthreads();
+  int cnt = 0;
+  for (int slot = tid; slot < N; slot += NT) {
+    const size_t i = row + (size_t)(s + slot);
+    const bool valid = slot < len && io.mask[i] != 0;
+    double e = 1.0;
+    if (valid) {
+      const float c = io.conf[i];
+      e = cand_eps(io.eps, c, i);
+      if constexpr (Robust) e = robust_eps(e, io.eta, i);
+      sh.conf[slot] = c;
+      sh.e[slot] = e;
+      ++cnt;
+    }
+    sh.key[slot] = sort_key(valid, e, slot);
+  }
+  if (cnt) atomicAdd(&sh.m, cnt);
+  __syncthreads();
+  const int nstar = select_wg<R, NT>(sh, N, param);
+  for (int slot = tid; slot < len; slot += NT) {
+    const size_t i = row + (size_t)(s + slot);
+    const bool take = sh.flag[slot] != 0;
+    if (io.commit) io.commit[i] = take ? 1 : 0;
+    if (take && io.x) {
+      io.x[i] = io.tokens[i];
+      io.mask[i] = 0;
+    }
+  }
+  if (io.n_commit && tid == 0) io.n_commit[b] = nstar;
 }
 
 // ---------------------------------------------------------------------------
@@ -632,10 +817,10 @@ k_fused(const typename Vec::Raw* __restrict__ logits, int B, int L, int nvec,
         uint8_t* __restrict__ mask, const int32_t* __restrict__ bstart,
         const int32_t* __restrict__ bend, int32_t* __restrict__ x, float param, EtaIn eta,
         RowOut out, uint8_t* __restrict__ commit, int32_t* __restrict__ n_commit) {
-  __shared__ int s_cand[kMaxBlock];       // candidate slots, compacted
-  __shared__ int s_tok[kMaxBlock];
-  __shared__ float s_conf[kMaxBlock];
-  __shared__ float s_eps[kMaxBlock];
+  __shared__ int s_cand[kWaveBlock];      // candidate slots, compacted
+  __shared__ int s_tok[kWaveBlock];
+  __shared__ float s_conf[kWaveBlock];
+  __shared__ float s_eps[kWaveBlock];
   __shared__ int s_m;
   const int b = blockIdx.x;
   const int wave = threadIdx.x / kWave;
@@ -692,6 +877,109 @@ k_fused(const typename Vec::Raw* __restrict__ logits, int B, int L, int nvec,
   if (n_commit && lane == 0) n_commit[b] = ok ? nstar : -1;
 }
 
+// Fused decode step for rows of more than 64 positions (blocks up to
+// kMaxBlock); the vocabulary pass is the same, the selection as in
+// k_select_wide.
+template <class Vec, int U, int W, int R, bool Robust>
+__global__ void __launch_bounds__(W * kWave)
+k_fused_wide(const typename Vec::Raw* __restrict__ logits, int B, int L, int nvec,
+             uint8_t* __restrict__ mask, const int32_t* __restrict__ bstart,
+             const int32_t* __restrict__ bend, int32_t* __restrict__ x, float param, EtaIn eta,
+             RowOut out, uint8_t* __restrict__ commit, int32_t* __restrict__ n_commit) {
+  constexpr int NT = W * kWave;
+  __shared__ WideLds sh;
+  __shared__ int s_cand[kMaxBlock];       // candidate slots, compacted
+  const int b = blockIdx.x;
+  const int tid = threadIdx.x;
+  const int wave = tid / kWave;
+  const int lane = tid % kWave;
+  const size_t row0 = (size_t)b * L;
+  const int s = bstart[b], e = bend[b];
+  const bool ok = window_ok(s, e, L);
+  const int len = ok ? e - s : 0;
+  if (wave == 0) {
+    int base = 0;
+    for (int c0 = 0; c0 < len; c0 += kWave) {
+      const int slot = c0 + lane;
+      const bool valid = slot < len && mask[row0 + s + slot] != 0;
+      const unsigned long long vm = __ballot(valid);
+      if (valid) s_cand[base + __popcll(vm & ((1ull << lane) - 1ull))] = slot;
+      base += __popcll(vm);
+    }
+    if (lane == 0) sh.m = base;
+  }
+  for (int q = tid; q < L; q += NT) {
+    const bool inwin = q >= s && q < s + len;
+    if (!inwin || mask[row0 + q] == 0) {
+      store_default(out, row0 + q);
+      if (commit) commit[row0 + q] = 0;
+    }
+  }
+  __syncthreads();
+  const int m = sh.m;
+  for (int c = wave; c < m; c += W) {
+    const int slot = s_cand[c];
+    const size_t r = row0 + s + slot;
+    const WavePartial wp = row_pass<Vec, U, 1>(logits + r * (size_t)nvec, nvec, 0);
+    const RowResult rr = finish_row(wp.m, wp.K, wp.S, wp.first);
+    if (lane == 0) {
+      store_row(out, r, rr);
+      sh.tok[slot] = rr.token;
+      sh.conf[slot] = rr.conf;
+      sh.e[slot] = (double)rr.eps;
+    }
+  }
+  __syncthreads();
+  if (len <= kWave) {
+    if (wave != 0) return;
+    const size_t i = row0 + (size_t)(s + lane);
+    const bool valid = lane < len && mask[i] != 0;
+    double ev = valid ? sh.e[lane] : 1.0;
+    if constexpr (Robust) {
+      if (valid) ev = robust_eps(ev, eta, i);
+    }
+    bool take = false;
+    const int nstar = select_wave<R>(valid, ev, valid ? sh.conf[lane] : 0.0f, param, take);
+    if (valid) {
+      if (commit) commit[i] = take ? 1 : 0;
+      if (take) {
+        x[i] = sh.tok[lane];
+        mask[i] = 0;
+      }
+    }
+    if (n_commit && lane == 0) n_commit[b] = ok ? nstar : -1;
+    return;
+  }
+  const int N = next_pow2(len);
+  for (int slot = tid; slot < N; slot += NT) {
+    const size_t i = row0 + (size_t)(s + slot);
+    const bool valid = slot < len && mask[i] != 0;
+    double ev = 1.0;
+    if (valid) {
+      ev = sh.e[slot];
+      if constexpr (Robust) {
+        ev = robust_eps(ev, eta, i);
+        sh.e[slot] = ev;
+      }
+    }
+    sh.key[slot] = sort_key(valid, ev, slot);
+  }
+  __syncthreads();
+  const int nstar = select_wg<R, NT>(sh, N, param);
+  for (int slot = tid; slot < len; slot += NT) {
+    const size_t i = row0 + (size_t)(s + slot);
+    if (mask[i] != 0) {
+      const bool take = sh.flag[slot] != 0;
+      if (commit) commit[i] = take ? 1 : 0;
+      if (take) {
+        x[i] = sh.tok[slot];
+        mask[i] = 0;
+      }
+    }
+  }
+  if (n_commit && tid == 0) n_commit[b] = nstar;
+}
+
 __global__ void __launch_bounds__(256) k_reveal(const uint8_t* __restrict__ commit,
                                                  const int32_t* __restrict__ tokens,
                                                  int32_t* __restrict__ x, uint8_t* __restrict__ mask,
@@ -722,7 +1010,7 @@ static Plan make_plan(int B, int L, int V, fdllm_dtype dt) {
   (void)V;
   (void)dt;
   Plan p{};
-  const long long win = L < kMaxBlock ? L : kMaxBlock;
+  const long long win = L < kWaveBlock ? L : kWaveBlock;   // typical block: one wavefront
   p.fused = B >= kFusedMinB;
   p.split = 1;
   if (!p.fused) {
@@ -778,22 +1066,24 @@ static hipError_t launch_confidence(const void* logits, fdllm_dtype dt, int B, i
   return launch_confidence_t<VecF32x1>(logits, B, L, V, split, mask, bs, be, out, st);
 }
 
+template <int R, bool Robust>
+static void launch_select_t(const SelectIO& io, int B, int L, float param, hipStream_t st) {
+  constexpr int kWideThreads = 256;
+  if (L <= kWaveBlock)
+    hipLaunchKernelGGL((k_select<R, Robust>), dim3((unsigned)((B + 3) / 4)), dim3(256), 0, st, io,
+                       B, L, param);
+  else
+    hipLaunchKernelGGL((k_select_wide<R, Robust, kWideThreads>), dim3((unsigned)B),
+                       dim3(kWideThreads), 0, st, io, B, L, param);
+}
+
 static hipError_t launch_select(fdllm_selector sel, const SelectIO& io, int B, int L, float param,
                                 hipStream_t st) {
-  const dim3 grid((unsigned)((B + 3) / 4)), block(256);
   switch (sel) {
-    case FDLLM_SEL_THRESHOLD:
-      hipLaunchKernelGGL((k_select<kThreshold, false>), grid, block, 0, st, io, B, L, param);
-      break;
-    case FDLLM_SEL_FACTOR:
-      hipLaunchKernelGGL((k_select<kFactor, false>), grid, block, 0, st, io, B, L, param);
-      break;
-    case FDLLM_SEL_ROBUST:
-      hipLaunchKernelGGL((k_select<kProfile, true>), grid, block, 0, st, io, B, L, param);
-      break;
-    default:
-      hipLaunchKernelGGL((k_select<kProfile, false>), grid, block, 0, st, io, B, L, param);
-      break;
+    case FDLLM_SEL_THRESHOLD: launch_select_t<kThreshold, false>(io, B, L, param, st); break;
+    case FDLLM_SEL_FACTOR: launch_select_t<kFactor, false>(io, B, L, param, st); break;
+    case FDLLM_SEL_ROBUST: launch_select_t<kProfile, true>(io, B, L, param, st); break;
+    default: launch_select_t<kProfile, false>(io, B, L, param, st); break;
   }
   return hipGetLastError();
 }
@@ -803,9 +1093,14 @@ static void launch_fused_t(const void* logits, int B, int L, int nvec, uint8_t* 
                            const int32_t* bs, const int32_t* be, int32_t* x, float param,
                            EtaIn eta, RowOut out, uint8_t* commit, int32_t* n_commit,
                            hipStream_t st) {
-  hipLaunchKernelGGL((k_fused<Vec, Vec::kU, kFusedWaves, R, Robust>), dim3((unsigned)B),
-                     dim3(kFusedWaves * kWave), 0, st, (const typename Vec::Raw*)logits, B, L, nvec,
-                     mask, bs, be, x, param, eta, out, commit, n_commit);
+  if (L <= kWaveBlock)
+    hipLaunchKernelGGL((k_fused<Vec, Vec::kU, kFusedWaves, R, Robust>), dim3((unsigned)B),
+                       dim3(kFusedWaves * kWave), 0, st, (const typename Vec::Raw*)logits, B, L,
+                       nvec, mask, bs, be, x, param, eta, out, commit, n_commit);
+  else
+    hipLaunchKernelGGL((k_fused_wide<Vec, Vec::kU, kFusedWaves, R, Robust>), dim3((unsigned)B),
+                       dim3(kFusedWaves * kWave), 0, st, (const typename Vec::Raw*)logits, B, L,
+                       nvec, mask, bs, be, x, param, eta, out, commit, n_commit);
 }
 
 template <class Vec>

@@ -20,6 +20,7 @@ import oracle
 CONF_RTOL = 1e-5
 LSE_RTOL = 1e-5
 EPS_RTOL = 1e-5
+MAX_BLOCK = 1024        # longest block the library accepts (FDLLM_MAX_BLOCK)
 
 
 def say(*a):
@@ -94,7 +95,7 @@ def oracle_confidence_subset(inp, bs: Sequence[int]):
 def check_defaults(g_tok, g_conf, g_eps, g_lse, mask, start, end, bs):
     for b in bs:
         for i in range(mask.shape[1]):
-            cand = int(start[b]) <= i < int(end[b]) and mask[b, i] and int(end[b]) - int(start[b]) <= 64
+            cand = int(start[b]) <= i < int(end[b]) and mask[b, i] and int(end[b]) - int(start[b]) <= MAX_BLOCK
             if not cand:
                 assert (int(g_tok[b, i]), float(g_conf[b, i]), float(g_eps[b, i]), float(g_lse[b, i])) \
                     == (-1, 0.0, 1.0, 0.0), (b, i)

@@ -111,3 +111,10 @@ def test_binding_refuses_cpu_tensors(lib):
 def test_missing_library_fails_loudly(tmp_path):
     with pytest.raises(FileNotFoundError):
         fd.load(str(tmp_path / "libfdllm.so"))
+
+
+def test_block_limit_agrees_with_header():
+    text = open(HEADER).read()
+    m = re.search(r"#define\s+FDLLM_MAX_BLOCK\s+(\d+)", text)
+    import parity
+    assert m and int(m.group(1)) == fd.MAX_BLOCK == parity.MAX_BLOCK

@@ -49,12 +49,21 @@ SMALL = [
     (129, 3, 7, torch.bfloat16, None),        # fused plan, scalar path
 ]
 
+# blocks beyond one wavefront (block-size ablation): workgroup selection
+WIDE = [
+    (3, 200, 1000, torch.bfloat16, 200),      # two-kernel plan
+    (2, 1024, 300, torch.float32, 1024),      # largest block
+    (130, 100, 64, torch.bfloat16, 100),      # fused plan
+    (129, 700, 40, torch.bfloat16, 700),
+    (128, 1024, 13, torch.float32, 1024),     # fused plan, scalar path, largest block
+]
+
 
 def _case(B, L, V, dt, window, seed=0):
     return workloads.random_case(B, L, V, dt, device="cuda", seed=seed, window=window)
 
 
-@pytest.mark.parametrize("B,L,V,dt,window", SMALL)
+@pytest.mark.parametrize("B,L,V,dt,window", SMALL + WIDE)
 def test_confidence_vs_oracle(gpu, B, L, V, dt, window):
     inp = _case(B, L, V, dt, window, seed=B * 7 + L)
     say(f"[confidence] {inp.name}")
@@ -67,7 +76,7 @@ def test_confidence_vs_oracle(gpu, B, L, V, dt, window):
     say(f"  {len(cells)} rows, worst rel err {worst}")
 
 
-@pytest.mark.parametrize("B,L,V,dt,window", SMALL[:6] + SMALL[8:9])
+@pytest.mark.parametrize("B,L,V,dt,window", SMALL[:6] + SMALL[8:9] + WIDE[:3])
 def test_select_vs_oracle_on_gpu_confidences(gpu, B, L, V, dt, window):
     inp = _case(B, L, V, dt, window, seed=B * 11 + L)
     say(f"[select] {inp.name}")
@@ -105,17 +114,18 @@ def _decode(gpu, inp, rule, p, with_outputs=True, eta=None, eta_uniform=0.0):
     return mask, x, outs
 
 
-@pytest.mark.parametrize("B,L,V,dt,window", SMALL)
+@pytest.mark.parametrize("B,L,V,dt,window", SMALL + WIDE)
 def test_decode_step_vs_oracle(gpu, B, L, V, dt, window):
     inp = _case(B, L, V, dt, window, seed=B * 13 + L)
     say(f"[decode] {inp.name}")
     m0, x0 = inp.mask.cpu().numpy(), inp.x.cpu().numpy()
     start, end = inp.start.cpu().numpy(), inp.end.cpu().numpy()
     ref_conf = gpu_confidence(gpu, inp)
+    rows = row_source(inp.logits.cpu())
     for rule, p in RULES:
         eta, eta_u, eta_o = _eta_for(rule, p, B, L, B * 3 + L)
         mask, x, o = _decode(gpu, inp, rule, p, eta=eta, eta_uniform=eta_u)
-        r = oracle.decode_step(row_source(inp.logits), B, L, m0, start, end, x0, rule, p, eta=eta_o)
+        r = oracle.decode_step(rows, B, L, m0, start, end, x0, rule, p, eta=eta_o)
         nf, nfm = compare_selection(o["commit"].cpu().numpy(), o["n_commit"].cpu().numpy(),
                                     r.commit, r.n_commit, r.flagged, range(B))
         ok = ~r.flagged
@@ -169,23 +179,25 @@ def test_crafted_profiles_on_gpu(gpu):
 
 def test_invalid_bounds_on_device(gpu):
     V = 64
-    for (BB, LL) in [(6, 20), (130, 100)]:
+    for (BB, LL) in [(6, 20), (130, 100), (7, 1100), (130, 1030)]:
         case = workloads.random_case(BB, LL, V, torch.bfloat16, device="cuda", seed=7, poison=False)
         s = torch.zeros(BB, dtype=torch.int32); e = torch.zeros(BB, dtype=torch.int32)
+        bounds = [(0, LL), (5, 4), (-1, 3), (0, LL + 1), (3, 3), (10, 10 + 65), (2, 2 + 1025)]
         for b in range(BB):
-            s[b], e[b] = [(0, LL), (5, 4), (-1, 3), (0, LL + 1), (3, 3), (10, 10 + 65)][b % 6]
+            s[b], e[b] = bounds[b % len(bounds)]
         case.start.copy_(s); case.end.copy_(e)
         say(f"[bounds] B={BB} L={LL}")
         mask, x, o = _decode(gpu, case, "profile", 1.0)
         n = o["n_commit"].cpu().numpy()
         for b in range(BB):
-            bad = b % 6 in (1, 2, 3, 5) or (b % 6 == 0 and LL > 64)
+            lo, hi = bounds[b % len(bounds)]
+            bad = not (0 <= lo <= hi <= LL and hi - lo <= gpu.MAX_BLOCK)
             if bad:
                 assert n[b] == -1
                 assert not o["commit"][b].any()
                 assert torch.equal(mask[b], case.mask[b]) and torch.equal(x[b], case.x[b])
                 assert (o["tokens"][b] == -1).all()
-            elif b % 6 == 4:
+            elif hi == lo:
                 assert n[b] == 0
 
 
@@ -211,3 +223,69 @@ def test_determinism_and_identical_rows(gpu):
         _, _, op = _decode(gpu, inp, "profile", f)
         _, _, of = _decode(gpu, inp, "factor", f)
         assert torch.equal(op["commit"], of["commit"]) and torch.equal(op["n_commit"], of["n_commit"])
+
+
+def _tied_profiles(B, L, seed):
+    """conf on a coarse grid (many exact ties) with a few large gaps."""
+    g = torch.Generator().manual_seed(seed)
+    q = torch.randint(40, 65, (B, L), generator=g).float() / 64
+    fine = torch.rand((B, L), generator=g) < 0.5
+    conf = torch.where(fine, 1 - torch.rand((B, L), generator=g) ** 3 * 0.05, q)
+    mask = (torch.rand((B, L), generator=g) < 0.8).to(torch.uint8)
+    return conf, mask
+
+
+@pytest.mark.parametrize("B,L", [(7, 1024), (130, 700)])
+def test_wide_blocks_select_vs_oracle(gpu, B, L):
+    """Windows from empty to 1024 slots, exact ties, both kernels' selection paths."""
+    conf, mask = _tied_profiles(B, L, seed=B + L)
+    spans = [(0, L), (0, 65), (L // 10, L - L // 7), (5, 5 + 64), (3, 3 + 128), (L - 777 % L, L),
+             (1, 1), (0, 1), (0, 63)]
+    start = torch.tensor([spans[b % len(spans)][0] for b in range(B)], dtype=torch.int32)
+    end = torch.tensor([min(spans[b % len(spans)][1], L) for b in range(B)], dtype=torch.int32)
+    eps = 1 - conf                                    # exact for these values
+    c_d, e_d, m_d, s_d, en_d = (t.cuda() for t in (conf, eps, mask, start, end))
+    eta = torch.rand((B, L), generator=torch.Generator().manual_seed(3)) * 0.05
+    say(f"[wide select] B={B} L={L}")
+    for use_eps in (True, False):
+        for rule, p in RULES:
+            eta_d = eta.cuda() if rule == "robust" and p == 1.0 else None
+            eta_u = 0.03 if rule == "robust" and p == 0.75 else 0.0
+            eta_o = eta.double().numpy() if eta_d is not None else (eta_u if rule == "robust" else None)
+            commit = torch.full((B, L), 9, dtype=torch.uint8, device="cuda")
+            n = torch.full((B,), -9, dtype=torch.int32, device="cuda")
+            gpu.select(rule, c_d, e_d if use_eps else None, m_d, s_d, en_d, p, commit, n,
+                       eta=eta_d, eta_uniform=eta_u)
+            torch.cuda.synchronize()
+            oc, on, flagged, _ = oracle.select(eps.double().numpy(), conf.double().numpy(),
+                                               mask.numpy(), start.numpy(), end.numpy(), rule, p,
+                                               eta=eta_o)
+            nf, nfm = compare_selection(commit.cpu().numpy(), n.cpu().numpy(), oc, on, flagged,
+                                        range(B))
+            say(f"  {rule}({p}) eps={use_eps}: flagged {nf} (matching {nfm})")
+
+
+@pytest.mark.parametrize("B", [3, 130])
+def test_wide_flat_block_profile_equals_factor(gpu, B):
+    """A block of 1024 identical rows: B_n = 0, so profile and factor agree bitwise."""
+    L, V = 1024, 256
+    g = torch.Generator(device="cuda").manual_seed(11)
+    one = torch.randn((1, 1, V), generator=g, device="cuda")
+    one[0, 0, 17] += 9.0
+    logits = one.expand(B, L, V).to(torch.bfloat16).contiguous()
+    mask = torch.ones((B, L), dtype=torch.uint8, device="cuda")
+    start = torch.zeros(B, dtype=torch.int32, device="cuda")
+    end = torch.full((B,), L, dtype=torch.int32, device="cuda")
+    x = torch.full((B, L), -1, dtype=torch.int32, device="cuda")
+    inp = workloads.StepInputs(logits, mask, start, end, x, "identical-wide")
+    say(f"[wide flat] B={B}")
+    for f in (0.5, 1.0, 2.0, 50.0):
+        _, _, op = _decode(gpu, inp, "profile", f)
+        _, _, of = _decode(gpu, inp, "factor", f)
+        assert torch.equal(op["commit"], of["commit"]) and torch.equal(op["n_commit"], of["n_commit"])
+        n = int(op["n_commit"][0])
+        e = float(op["eps"][0, 0])
+        want = max([k for k in range(1, L + 1) if (k + 1) * e < f] or [1])
+        assert (op["n_commit"] == n).all() and n == want, (n, want)
+        # ties go to the lower positions: the first n* slots commit
+        assert int(op["commit"][:, :n].sum()) == B * n and int(op["commit"][:, n:].sum()) == 0

@@ -96,8 +96,8 @@ SELECT_MUTANTS = {
 
 
 def _frechet_variant(kind):
-    def fq(eps_sorted):
-        out = _FRECHET_Q(eps_sorted)
+    def fq(eps_sorted, with_bonus=True):
+        out = _FRECHET_Q(eps_sorted, with_bonus)
         for q in out:
             n = q["n"]
             c = [1 - Q(e) for e in eps_sorted]
