@@ -12,13 +12,21 @@ step does the same work.
 
 Prints one JSON line.  `value` is masked positions per second over the whole
 timed region; `roofline` relates the fused kernel's algorithmic bytes to its
-average launch time measured with HIP events on the launch stream.
+average launch time measured with HIP events on the launch stream, and to a
+read-only stream of the same logits buffer (libfdllm_bench.so).
+`cpu_baseline` times the CPU oracle on a bounded sample of the same workload:
+on all host cores (one process per core, each on its own sequences) and on
+one core.  `--per-config` adds the other workload recipes (one sequence fp32;
+eight-sequence and 256-sequence simulated generations; 64 sequences in a
+512-position span), cold and cache-hot, and can write them as a markdown
+table.
 """
 from __future__ import annotations
 
 import argparse
 import hashlib
 import json
+import multiprocessing as mp
 import os
 import sys
 import time
@@ -31,6 +39,11 @@ HBM_PEAK_GBPS = 8000.0
 IO_BYTES_PER_POSITION = 18   # mask read, commit, tokens, conf, eps, lse (1+1+4+4+4+4)
 SRC = os.path.join(ROOT, "paper_2606_02955_amd", "csrc", "fdllm.hip")
 TRAFFIC = os.path.join(ROOT, "profiles", "traffic_fused_decode_config5.json")
+MAX_HOST_WORKERS = 16        # host CPU share of one GPU
+
+
+def log(msg: str):
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
 
 
 def source_digest() -> str:
@@ -48,9 +61,98 @@ def measured_traffic():
     return t.get("hbm_bytes_per_launch")
 
 
-def cpu_baseline(inp, n_blocks: int, rule: str, param: float):
-    """The oracle on a bounded, seeded sample of blocks of the same step."""
+def cpu_model() -> str:
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def under_profiler() -> bool:
+    return "rocprof" in os.environ.get("LD_PRELOAD", "") or any(
+        k.startswith("ROCPROF") for k in os.environ)
+
+
+# ---------------------------------------------------------------------------
+# CPU oracle on all host cores: one spawned process per core, CPU only.  The
+# processes start before this process touches the GPU, build their own
+# sequences of the same recipe on the CPU, report ready, and run the oracle
+# when released; the parallel time is last finish minus first start.
+# ---------------------------------------------------------------------------
+def _oracle_worker(blocks, rule, param, ready, go, results):
     import numpy as np
+    import torch
+    torch.set_num_threads(1)
+    import oracle
+    import workloads
+    rows = torch.stack([workloads.config5_rows(b, "cpu") for b in blocks])     # [n, L, V] bf16
+    n, L, _ = rows.shape
+    mask = np.ones((n, L), dtype=np.uint8)
+    start = np.zeros(n, dtype=np.int64)
+    end = np.full(n, L, dtype=np.int64)
+    x = np.full((n, L), -1, dtype=np.int64)
+    get = lambda b, i: rows[b, i].to(torch.float64).numpy()
+    ready.put(os.getpid())
+    go.wait()
+    t0 = time.time()
+    r = oracle.decode_step(get, n, L, mask, start, end, x, rule, param)
+    t1 = time.time()
+    results.put((t0, t1, int(mask.sum()), int(r.n_commit.sum())))
+
+
+class OracleCrew:
+    def __init__(self, n_workers: int, blocks_per_worker: int, rule: str, param: float):
+        ctx = mp.get_context("spawn")
+        self.ready, self.results, self.go = ctx.Queue(), ctx.Queue(), ctx.Event()
+        self.bpw = blocks_per_worker
+        self.procs = [ctx.Process(target=_oracle_worker,
+                                  args=(list(range(w * blocks_per_worker, (w + 1) * blocks_per_worker)),
+                                        rule, param, self.ready, self.go, self.results), daemon=True)
+                      for w in range(n_workers)]
+        for p in self.procs:
+            p.start()
+
+    def _collect(self, q, timeout: float):
+        """One item per process from q; raises if a process died or time ran out."""
+        import queue
+        items, deadline = [], time.time() + timeout
+        while len(items) < len(self.procs):
+            try:
+                items.append(q.get(timeout=1.0))
+            except queue.Empty:
+                dead = [p.exitcode for p in self.procs if p.exitcode not in (None, 0)]
+                if dead:
+                    raise RuntimeError(f"oracle process exited with status {dead[0]}")
+                if time.time() > deadline:
+                    raise TimeoutError("oracle processes did not finish in time")
+        return items
+
+    def wait_ready(self, timeout: float):
+        self._collect(self.ready, timeout)
+
+    def run(self, timeout: float):
+        self.go.set()
+        res = self._collect(self.results, timeout)
+        for p in self.procs:
+            p.join(timeout=30)
+        t0 = min(r[0] for r in res)
+        t1 = max(r[1] for r in res)
+        return t1 - t0, sum(r[2] for r in res), sum(r[3] for r in res), max(r[1] - r[0] for r in res)
+
+    def stop(self):
+        for p in self.procs:
+            if p.is_alive():
+                p.terminate()
+                p.join(timeout=10)
+
+
+def cpu_baseline_single(inp, n_blocks: int, rule: str, param: float):
+    """The oracle on one core, on a seeded sample of blocks of the timed step."""
+    import numpy as np
+    import torch
     import oracle
     B, L, V = inp.logits.shape
     rng = np.random.default_rng(7)
@@ -59,17 +161,151 @@ def cpu_baseline(inp, n_blocks: int, rule: str, param: float):
     mask = inp.mask[blocks].cpu().numpy()
     start, end = inp.start[blocks].cpu().numpy(), inp.end[blocks].cpu().numpy()
     x = inp.x[blocks].cpu().numpy()
-    get = lambda b, i: rows[b, i].to(dtype=__import__("torch").float64).numpy()
+    get = lambda b, i: rows[b, i].to(dtype=torch.float64).numpy()
     t0 = time.perf_counter()
     r = oracle.decode_step(get, n_blocks, L, mask, start, end, x, rule, param)
     dt = time.perf_counter() - t0
     n_pos = int(mask.sum())
     return {"value": n_pos / dt, "unit": "masked positions/s", "cores": 1, "kind": "oracle",
             "sample": f"{n_blocks} of {B} blocks ({n_pos} positions, {n_pos * V * 2 / 1e9:.2f} GB of "
-                      f"bf16 logits) of the same step, {rule} f={param}; single-threaded NumPy "
-                      f"float64 + exact rational selection; {dt:.1f} s",
-            "seconds": dt, "host_cpus_available": len(os.sched_getaffinity(0)),
-            "commits": int(r.n_commit.sum())}
+                      f"bf16 logits) of the timed step, {rule} f={param}; one process, NumPy float64 "
+                      f"+ exact rational selection; {dt:.1f} s",
+            "seconds": dt, "logits_GBps": n_pos * V * 2 / dt / 1e9, "commits": int(r.n_commit.sum())}
+
+
+# ---------------------------------------------------------------------------
+# per-configuration report
+# ---------------------------------------------------------------------------
+def _candidates(inp) -> int:
+    import torch
+    L = inp.logits.shape[1]
+    pos = torch.arange(L, device=inp.mask.device).view(1, L)
+    inwin = (pos >= inp.start.view(-1, 1)) & (pos < inp.end.view(-1, 1))
+    return int((inwin & inp.mask.bool()).sum())
+
+
+def _time_steps(fd, torch, inp, selector, p, reps, scratch=None):
+    """Average decode-step kernel time (HIP events) over reps, input state restored."""
+    B = inp.logits.shape[0]
+    mask0, x0 = inp.mask.clone(), inp.x.clone()
+    mask, x = mask0.clone(), x0.clone()
+    nc = torch.empty((B,), dtype=torch.int32, device=inp.logits.device)
+    ws = fd.fdllm_decode_step(inp.logits, mask, inp.start, inp.end, x, selector, p, n_commit=nc)
+    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+           for _ in range(reps)]
+    for k in range(reps):
+        mask.copy_(mask0)
+        x.copy_(x0)
+        if scratch is not None:
+            scratch.fill_(k & 0x7F)          # evicts the logits from L2 and the Infinity Cache
+        evs[k][0].record()
+        fd.fdllm_decode_step(inp.logits, mask, inp.start, inp.end, x, selector, p, n_commit=nc,
+                             workspace=ws)
+        evs[k][1].record()
+    torch.cuda.synchronize()
+    t = sorted(a.elapsed_time(b) * 1e-3 for a, b in evs)
+    return sum(t) / len(t), t[len(t) // 2], float(nc.clamp(min=0).float().mean())
+
+
+def _row(name, shape, sel, positions, bytes_, t_cold, t_hot, stream_gbps, extra=None):
+    d = {"config": name, "shape": shape, "selector": sel, "positions_per_step": positions,
+         "logits_bytes_per_step": bytes_, "kernel_ms_cold": 1e3 * t_cold,
+         "kernel_ms_hot": None if t_hot is None else 1e3 * t_hot,
+         "positions_per_s": positions / t_cold, "logits_GBps": bytes_ / t_cold / 1e9,
+         "frac_of_peak": bytes_ / t_cold / 1e9 / HBM_PEAK_GBPS,
+         "frac_of_stream": bytes_ / t_cold / 1e9 / stream_gbps if stream_gbps else None}
+    if extra:
+        d.update(extra)
+    return d
+
+
+def per_config_report(fd, torch, workloads, dev, stream_gbps, reps):
+    import gc
+    rows = []
+    scratch = torch.empty(512 << 20, dtype=torch.uint8, device=dev)
+    sels = {k: [(s, p) for s in v["selectors"] for p in v["params"][s]]
+            for k, v in workloads.CONFIGS.items()}
+
+    def static(k, inp, label, cold_needed=True):
+        B, L, V = inp.logits.shape
+        pos = _candidates(inp)
+        nbytes = pos * V * inp.logits.element_size()
+        for sel, p in sels[k]:
+            tc, _, commits = _time_steps(fd, torch, inp, sel, p, reps, scratch if cold_needed else None)
+            th = _time_steps(fd, torch, inp, sel, p, reps)[0] if cold_needed else None
+            extra = {"mean_commits_per_block": commits}
+            if not cold_needed:
+                extra["note"] = "cold by size: the step reads far more than the caches hold"
+            rows.append(_row(k, label, f"{sel}({p})", pos, nbytes, tc, th, stream_gbps, extra))
+            log(f"config{k} {sel}({p}): {1e3 * tc:.3f} ms cold, {nbytes / tc / 1e9:.0f} GB/s")
+
+    log("per-config: config1")
+    inp = workloads.config1(device=dev)
+    static(1, inp, "B=1 L=32 V=126464 fp32")
+    del inp
+    log("per-config: config3")
+    inp = workloads.config3(device=dev)
+    static(3, inp, "B=64 span 512, m_b~U{1..32}, V=126464 bf16")
+    del inp
+    gc.collect()
+    torch.cuda.empty_cache()
+    # config2: whole simulated generations, one per selector
+    for sel, p in sels[2]:
+        gen = workloads.SimulatedGeneration(2, device=dev)
+        nc = torch.empty((gen.B,), dtype=torch.int32, device=dev)
+        steps, commits, positions, ktime, ws = 0, 0, 0, 0.0, None
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        while not gen.done() and steps < 4096:
+            inp = gen.prepare_step()
+            positions += _candidates(inp)
+            e0.record()
+            ws = fd.fdllm_decode_step(inp.logits, inp.mask, inp.start, inp.end, inp.x, sel, p,
+                                      n_commit=nc, workspace=ws)
+            e1.record()
+            torch.cuda.synchronize()
+            ktime += e0.elapsed_time(e1) * 1e-3
+            commits += int(nc.clamp(min=0).sum())
+            steps += 1
+        nbytes = positions * gen.V * 2
+        rows.append(_row(2, "B=8 gen 256 in blocks of 32, V=126464 bf16 (whole generation)",
+                         f"{sel}({p})", positions / steps, nbytes / steps, ktime / steps, None,
+                         stream_gbps, {"steps": steps, "commits_per_step": commits / steps,
+                                       "note": "hot: each step's rows were just written"}))
+        log(f"config2 {sel}({p}): {steps} steps, {commits / steps:.2f} commits/step")
+        del gen
+    gc.collect()
+    torch.cuda.empty_cache()
+    log("per-config: config4 (first step of the generation)")
+    gen = workloads.SimulatedGeneration(4, device=dev)
+    inp = gen.prepare_step()
+    static(4, inp, "B=256 span 1024 (66 GB allocated), block 64, V=126464 bf16", cold_needed=False)
+    del inp, gen
+    gc.collect()
+    torch.cuda.empty_cache()
+    del scratch
+    return rows
+
+
+def per_config_markdown(rows, c5, stream_gbps, cmd) -> str:
+    out = ["# Decode-step throughput per workload recipe (one MI355X)", "",
+           "Command (from the repository root):", "", f"    {cmd}", "",
+           f"Read-only stream reference (`fdllm_stream_read` over the 8.29 GB logits buffer): "
+           f"{stream_gbps:.0f} GB/s.  Kernel times are HIP-event averages of `fdllm_decode_step`; "
+           "`cold` overwrites a 512 MB buffer before every step (evicting L2 and the Infinity "
+           "Cache), `hot` does not.  The per-step traffic of config2 is 8x32 rows, so its steps "
+           "are launch-bound.", "",
+           "| config | shape | selector | positions/step | kernel ms (cold) | kernel ms (hot) | "
+           "positions/s | logits GB/s | % of 8 TB/s | % of stream | commits |",
+           "|---|---|---|---|---|---|---|---|---|---|---|"]
+    for r in rows + c5:
+        hot = f"{r['kernel_ms_hot']:.4f}" if r["kernel_ms_hot"] is not None else "—"
+        commits = (f"{r['commits_per_step']:.2f}/step, {r['steps']} steps" if "steps" in r
+                   else f"{r.get('mean_commits_per_block', 0):.2f}/block")
+        fs = f"{100 * r['frac_of_stream']:.1f}" if r["frac_of_stream"] else "—"
+        out.append(f"| {r['config']} | {r['shape']} | {r['selector']} | {r['positions_per_step']:.0f} | "
+                   f"{r['kernel_ms_cold']:.4f} | {hot} | {r['positions_per_s']:.4g} | "
+                   f"{r['logits_GBps']:.0f} | {100 * r['frac_of_peak']:.1f} | {fs} | {commits} |")
+    return "\n".join(out) + "\n"
 
 
 def main():
@@ -79,9 +315,14 @@ def main():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--selector", default="profile", choices=["profile", "factor", "threshold"])
     ap.add_argument("--param", type=float, default=None, help="f (default 1.0) or tau (default 0.9)")
-    ap.add_argument("--cpu-blocks", type=int, default=40, help="blocks in the oracle sample")
+    ap.add_argument("--cpu-blocks", type=int, default=90, help="blocks in the one-core oracle sample")
+    ap.add_argument("--cpu-workers", type=int, default=0,
+                    help="processes of the all-core oracle run (0: host CPUs, at most 16)")
+    ap.add_argument("--cpu-worker-blocks", type=int, default=60, help="blocks per oracle process")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-selector-sweep", action="store_true")
+    ap.add_argument("--per-config", action="store_true", help="also time the other workload recipes")
+    ap.add_argument("--per-config-md", default=None, help="write the per-config table here")
     ap.add_argument("--copy-calibration-mb", type=int, default=1024,
                     help="size of a plain device copy timed (and counted by rocprofv3) for reference")
     args = ap.parse_args()
@@ -92,6 +333,18 @@ def main():
         sys.exit(2)
     param = args.param if args.param is not None else (0.9 if args.selector == "threshold" else 1.0)
 
+    crew, crew_note = None, None
+    if not args.no_cpu_baseline:
+        if under_profiler():
+            crew_note = "all-core oracle run skipped under a profiler"
+        else:
+            n_w = args.cpu_workers or min(MAX_HOST_WORKERS, len(os.sched_getaffinity(0)))
+            try:
+                crew = OracleCrew(n_w, args.cpu_worker_blocks, args.selector, param)
+                log(f"cpu_baseline: started {n_w} oracle processes")
+            except Exception as e:          # no process support: one-core figure only
+                crew_note = f"all-core oracle run unavailable: {e!r}"
+
     import torch
     import paper_2606_02955_amd as fd
     import workloads
@@ -99,8 +352,8 @@ def main():
     fd.load()
     dev = torch.device("cuda", 0)
     torch.cuda.set_device(dev)
-    print(f"[bench] generating config5 inputs on {torch.cuda.get_device_name(dev)}", file=sys.stderr, flush=True)
-    inp = workloads.config5(device=dev, progress=lambda m: print(f"[bench] {m}", file=sys.stderr, flush=True))
+    log(f"generating config5 inputs on {torch.cuda.get_device_name(dev)}")
+    inp = workloads.config5(device=dev, progress=log)
     B, L, V = inp.logits.shape
     positions = int(inp.mask.sum())
     logits_bytes = positions * V * inp.logits.element_size()
@@ -134,6 +387,28 @@ def main():
                     "read_plus_write_GBps": 2 * n / t / 1e9}
         del src, dst
 
+    # read-only stream of the same logits buffer: the measured bandwidth ceiling
+    sink = torch.zeros(1, dtype=torch.int32, device=dev)
+    fd.fdllm_stream_read(inp.logits, sink)
+    sevs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+            for _ in range(5)]
+    for a, b in sevs:
+        a.record()
+        fd.fdllm_stream_read(inp.logits, sink)
+        b.record()
+    torch.cuda.synchronize()
+    stream_s = sum(a.elapsed_time(b) for a, b in sevs) * 1e-3 / len(sevs)
+    stream_bytes = inp.logits.numel() * inp.logits.element_size()
+    stream_gbps = stream_bytes / stream_s / 1e9
+    log(f"stream read: {stream_gbps:.0f} GB/s")
+
+    if crew is not None:
+        try:
+            crew.wait_ready(timeout=600)    # no host load from the crew during GPU timing
+        except Exception as e:
+            crew.stop()
+            crew, crew_note = None, f"all-core oracle run unavailable: {e!r}"
+
     def run(selector, p, steps, warmup, label):
         evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
                for _ in range(steps)]
@@ -141,7 +416,7 @@ def main():
             mask.copy_(mask0); x.copy_(x0)
             fd.fdllm_decode_step(inp.logits, mask, inp.start, inp.end, x, selector, p, **outs)
         torch.cuda.synchronize()
-        print(f"[bench] {label}: timing {steps} steps", file=sys.stderr, flush=True)
+        log(f"{label}: timing {steps} steps")
         t0 = time.perf_counter()
         for k in range(steps):
             mask.copy_(mask0); x.copy_(x0)
@@ -156,15 +431,20 @@ def main():
     wall, kavg, kmin = run(args.selector, param, args.steps, args.warmup, f"{args.selector}({param})")
     commits = float(outs["n_commit"].float().mean())
     sweep = {}
+    c5_rows = [_row(5, "B=1024 L=32 V=126464 bf16", f"{args.selector}({param})", positions,
+                    logits_bytes, kavg, None, stream_gbps, {"mean_commits_per_block": commits})]
     if not args.no_selector_sweep:
         for sel, p in [("profile", 1.0), ("profile", 0.75), ("factor", 1.0), ("factor", 0.75),
                        ("threshold", 0.9)]:
             if sel == args.selector and p == param:
                 continue
-            w2, k2, _ = run(sel, p, max(5, args.steps // 4), 1, f"{sel}({p})")
-            sweep[f"{sel}({p})"] = {"ms_per_step": 1e3 * w2 / max(5, args.steps // 4),
-                                    "kernel_ms": 1e3 * k2,
-                                    "mean_commits_per_block": float(outs["n_commit"].float().mean())}
+            n2 = max(5, args.steps // 4)
+            w2, k2, _ = run(sel, p, n2, 1, f"{sel}({p})")
+            mc = float(outs["n_commit"].float().mean())
+            sweep[f"{sel}({p})"] = {"ms_per_step": 1e3 * w2 / n2, "kernel_ms": 1e3 * k2,
+                                    "mean_commits_per_block": mc}
+            c5_rows.append(_row(5, "B=1024 L=32 V=126464 bf16", f"{sel}({p})", positions,
+                                logits_bytes, k2, None, stream_gbps, {"mean_commits_per_block": mc}))
     ms = 1e3 * wall / args.steps
     value = positions * args.steps / wall
     achieved = algo_bytes / kavg / 1e9
@@ -196,14 +476,46 @@ def main():
                      "frac": achieved / HBM_PEAK_GBPS,
                      "traffic": traffic,
                      "kernel": "k_fused (one launch per step)",
-                     "algorithmic_bytes_per_launch": algo_bytes},
+                     "algorithmic_bytes_per_launch": algo_bytes,
+                     "stream_read_GBps": stream_gbps,
+                     "frac_of_stream_read": achieved / stream_gbps},
         "selectors": sweep,
         "copy_reference": copy_ref,
         "source_sha256_16": source_digest(),
     }
+    if args.per_config:
+        rows = per_config_report(fd, torch, workloads, dev, stream_gbps, reps=10)
+        line["per_config"] = rows + c5_rows
+        if args.per_config_md:
+            cmd = "python bench.py " + " ".join(sys.argv[1:])
+            with open(args.per_config_md, "w") as fh:
+                fh.write(per_config_markdown(rows, c5_rows, stream_gbps, cmd))
     if not args.no_cpu_baseline:
-        print(f"[bench] cpu_baseline: oracle on {args.cpu_blocks} blocks", file=sys.stderr, flush=True)
-        line["cpu_baseline"] = cpu_baseline(inp, args.cpu_blocks, args.selector, param)
+        log(f"cpu_baseline: oracle on {args.cpu_blocks} blocks, one core")
+        single = cpu_baseline_single(inp, args.cpu_blocks, args.selector, param)
+        single["cpu_model"] = cpu_model()
+        base = dict(single)
+        if crew is not None:
+            log(f"cpu_baseline: oracle on {len(crew.procs)} processes")
+            try:
+                wall_c, pos_c, commits_c, slowest = crew.run(timeout=900)
+                base = {"value": pos_c / wall_c, "unit": "masked positions/s",
+                        "cores": len(crew.procs), "kind": "oracle",
+                        "sample": f"{len(crew.procs)} processes x {crew.bpw} sequences of the same "
+                                  f"recipe built on the CPU ({pos_c} positions, "
+                                  f"{pos_c * V * 2 / 1e9:.2f} GB of bf16 logits), {args.selector} "
+                                  f"f={param}; NumPy float64 + exact rational selection; "
+                                  f"{wall_c:.1f} s from first start to last finish",
+                        "seconds": wall_c, "logits_GBps": pos_c * V * 2 / wall_c / 1e9,
+                        "commits": commits_c, "cpu_model": cpu_model(), "single_core": single}
+            except Exception as e:
+                base["note"] = f"all-core oracle run failed: {e!r}"
+            finally:
+                crew.stop()
+        elif crew_note:
+            base["note"] = crew_note
+        base["host_cpus_available"] = len(os.sched_getaffinity(0))
+        line["cpu_baseline"] = base
     else:
         line["cpu_baseline"] = None
     print(json.dumps(line), flush=True)

@@ -16,6 +16,7 @@ import torch
 
 _PKG = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_PKG, "libfdllm.so")
+BENCH_LIB_PATH = os.path.join(_PKG, "libfdllm_bench.so")
 
 BF16, F32 = 0, 1
 SEL_THRESHOLD, SEL_FACTOR, SEL_PROFILE, SEL_ROBUST = 0, 1, 2, 3
@@ -30,7 +31,10 @@ EXPORTS = ("fdllm_confidence", "fdllm_select_profile", "fdllm_select_factor",
            "fdllm_select_threshold", "fdllm_select_robust", "fdllm_reveal", "fdllm_decode_step",
            "fdllm_workspace_size", "fdllm_status_string")
 
+BENCH_EXPORTS = ("fdllm_stream_read",)
+
 _lib = None
+_bench_lib = None
 
 
 class FdllmError(RuntimeError):
@@ -208,3 +212,30 @@ def select(selector: str, conf, eps, mask, block_start, block_end, param, commit
     {"profile": fdllm_select_profile, "factor": fdllm_select_factor,
      "threshold": fdllm_select_threshold}[selector](conf, eps, mask, block_start, block_end,
                                                     param, commit, n_commit)
+
+
+def load_bench(path: Optional[str] = None) -> ctypes.CDLL:
+    """Load libfdllm_bench.so (the read-only stream reference); raises if absent."""
+    global _bench_lib
+    if _bench_lib is not None and path is None:
+        return _bench_lib
+    p = path or BENCH_LIB_PATH
+    if not os.path.exists(p):
+        raise FileNotFoundError(
+            f"{p} is missing: build it first (python -m paper_2606_02955_amd.build)")
+    lib = ctypes.CDLL(p)
+    lib.fdllm_stream_read.argtypes = [ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p,
+                                      ctypes.c_void_p]
+    lib.fdllm_stream_read.restype = ctypes.c_int
+    if path is None:
+        _bench_lib = lib
+    return lib
+
+
+def fdllm_stream_read(buf: torch.Tensor, sink: torch.Tensor):
+    """Read every byte of `buf` once (bandwidth reference; see fdllm_bench.h)."""
+    nbytes = buf.numel() * buf.element_size()
+    st = load_bench().fdllm_stream_read(_ptr(buf, name="buf"), nbytes,
+                                        _ptr(sink, torch.int32, (1,), "sink"), _stream(buf.device))
+    if st != 0:
+        raise RuntimeError(f"fdllm_stream_read: status {st}")

@@ -1,4 +1,9 @@
-"""Build the HIP library libfdllm.so in-tree for gfx950 (hipcc, no JIT)."""
+"""Build the HIP libraries in-tree for gfx950 (hipcc, no JIT).
+
+libfdllm.so is the commit selector (include/fdllm.h); libfdllm_bench.so is
+the read-only HBM stream used as the bandwidth reference in reports
+(include/fdllm_bench.h).
+"""
 from __future__ import annotations
 
 import os
@@ -11,6 +16,8 @@ ROOT = os.path.dirname(PKG)
 SRC = os.path.join(PKG, "csrc", "fdllm.hip")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(PKG, "libfdllm.so")
+BENCH_SRC = os.path.join(PKG, "csrc", "stream_read.hip")
+BENCH_LIB = os.path.join(PKG, "libfdllm_bench.so")
 ARCH = "gfx950"
 
 HIPCC_FLAGS = [
@@ -34,18 +41,23 @@ def hipcc() -> str:
     raise RuntimeError("hipcc not found (ROCm is required to build libfdllm.so)")
 
 
-def build(verbose: bool = False, extra=()) -> str:
-    """Compile csrc/fdllm.hip into libfdllm.so (always recompiles)."""
-    tmp = LIB + ".tmp"
-    cmd = [hipcc(), *HIPCC_FLAGS, *extra, "-I", INCLUDE, SRC, "-o", tmp]
+def _compile(src: str, lib: str, verbose: bool, extra=()) -> str:
+    tmp = lib + ".tmp"
+    cmd = [hipcc(), *HIPCC_FLAGS, *extra, "-I", INCLUDE, src, "-o", tmp]
     if verbose:
         print(" ".join(cmd), flush=True)
     res = subprocess.run(cmd, capture_output=True, text=True)
     if res.returncode != 0:
         sys.stderr.write(res.stdout + res.stderr)
-        raise RuntimeError(f"hipcc failed with status {res.returncode}")
-    os.replace(tmp, LIB)
-    return LIB
+        raise RuntimeError(f"hipcc failed with status {res.returncode} on {src}")
+    os.replace(tmp, lib)
+    return lib
+
+
+def build(verbose: bool = False, extra=()) -> str:
+    """Compile libfdllm.so and libfdllm_bench.so (always recompiles both)."""
+    _compile(BENCH_SRC, BENCH_LIB, verbose)
+    return _compile(SRC, LIB, verbose, extra)
 
 
 if __name__ == "__main__":

@@ -4,7 +4,7 @@
 //   (1) vocabulary pass: per candidate position, the greedy token, its softmax
 //       confidence c, the complement eps = 1 - c and the log-sum-exp
 //       (Sec. 3 "Notation"); every logit of a candidate row is read once;
-//   (2) selection: per block, sort the <= 64 candidates by confidence and
+//   (2) selection: per block, sort the candidates by confidence and
 //       apply the Frechet profile / factor / threshold rule (Sec. 3
 //       "Frechet profile quantities", Sec. 2, Sec. 5 "Baselines");
 //   (3) reveal: write the chosen tokens into the sequence and clear their mask.
@@ -30,11 +30,13 @@
 //   * wavefront reductions use DPP row operations, ds_swizzle and
 //     v_readlane; partials of a split row meet in LDS in fixed order, so
 //     results do not depend on scheduling.
-// The selection runs in one wavefront per block: a 64-lane bitonic sort of
-// (eps, slot) keys, a double-precision prefix scan of the heterogeneity
-// bonus, a ballot for n*, and ds_permute to route each decision back to its
-// position.  The calibration-robust rule (the appendix on calibration-robust
-// certificates) is the profile rule on eps_low = min(1, eps + eta).
+// A block of up to 64 positions is selected in one wavefront: a 64-lane
+// bitonic sort of (eps, slot) keys, a double-precision prefix scan of the
+// heterogeneity bonus, a ballot for n*, and ds_permute to route each decision
+// back to its position.  Longer blocks (up to 1024 positions) sort the same
+// keys in LDS across a workgroup with a fixed-order scan.  The
+// calibration-robust rule (the appendix on calibration-robust certificates)
+// is the profile rule on eps_low = min(1, eps + eta).
 #include <hip/hip_runtime.h>
 
 #include <math.h>
@@ -52,6 +54,9 @@
 #endif
 #ifndef FDLLM_U_F32
 #define FDLLM_U_F32 4
+#endif
+#ifndef FDLLM_TARGET_WAVES
+#define FDLLM_TARGET_WAVES 16384  // small batches: split rows until about this many waves stream
 #endif
 #ifndef FDLLM_WAVES_PER_EU
 #define FDLLM_WAVES_PER_EU 0   // minimum waves per SIMD the fused kernel is compiled for (0: no hint)
@@ -1004,7 +1009,7 @@ struct Plan {
 
 constexpr int kFusedMinB = 128;
 constexpr int kFusedWaves = FDLLM_FUSED_WAVES;   // waves per workgroup in the fused kernel
-constexpr int kTargetWaves = 2048;   // 8 per CU on 256 CUs
+constexpr int kTargetWaves = FDLLM_TARGET_WAVES;   // row-streaming waves the split aims for
 
 static Plan make_plan(int B, int L, int V, fdllm_dtype dt) {
   (void)V;

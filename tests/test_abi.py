@@ -12,8 +12,11 @@ ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 HEADER = os.path.join(ROOT, "include", "fdllm.h")
 
 
-def declared_functions():
-    text = open(HEADER).read()
+BENCH_HEADER = os.path.join(ROOT, "include", "fdllm_bench.h")
+
+
+def declared_functions(header=HEADER):
+    text = open(header).read()
     text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
     return sorted(set(re.findall(r"\b(fdllm_[a-z_]+)\s*\(", text)))
 
@@ -118,3 +121,15 @@ def test_block_limit_agrees_with_header():
     m = re.search(r"#define\s+FDLLM_MAX_BLOCK\s+(\d+)", text)
     import parity
     assert m and int(m.group(1)) == fd.MAX_BLOCK == parity.MAX_BLOCK
+
+
+def test_bench_library_exports_and_checks(lib):
+    blib = fd.load_bench()
+    names = declared_functions(BENCH_HEADER)
+    assert set(names) == set(fd.BENCH_EXPORTS), names
+    p = ctypes.c_void_p(0x1000)
+    assert blib.fdllm_stream_read(None, 0, None, None) == 0          # empty: no-op
+    assert blib.fdllm_stream_read(None, 32, p, None) == -1
+    assert blib.fdllm_stream_read(p, 32, None, None) == -1
+    assert blib.fdllm_stream_read(p, 24, p, None) == -1              # not a multiple of 16
+    assert blib.fdllm_stream_read(ctypes.c_void_p(0x1008), 32, p, None) == -1   # misaligned

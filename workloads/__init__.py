@@ -290,6 +290,21 @@ def config3(device="cpu", V: int = V_LLADA, B: int = 64, G: int = 512, blk: int 
 # config 5: throughput stress. B=1024, L=32, all masked, bf16 Gumbel(0,1)
 # background; 10% of positions carry a planted pair with gap U(0,1e-3).
 # ---------------------------------------------------------------------------
+def config5_rows(b: int, device="cpu", V: int = V_LLADA, L: int = 32) -> torch.Tensor:
+    """The [L, V] bf16 logits of sequence b (its own seeded stream per device)."""
+    g = _gen(5, 0, b, device)
+    rows = _gumbel(g, (L, V), device)
+    tie = torch.rand((L,), generator=g, device=device) < 0.10
+    toks = _distinct_tokens(g, L, 2, V, device)
+    H = _uniform(g, (L, 1), 13.0, 17.0, device)
+    gap = _uniform(g, (L, 1), 0.0, 1e-3, device)
+    idx = torch.nonzero(tie).flatten()
+    if idx.numel():
+        pair = torch.cat([H[idx], H[idx] - gap[idx]], 1)
+        rows[idx] = rows[idx].scatter(1, toks[idx], pair)
+    return rows.to(torch.bfloat16)
+
+
 def config5(device="cpu", V: int = V_LLADA, B: int = 1024, L: int = 32,
             chunk: int = 32, progress: Optional[Callable[[str], None]] = None) -> StepInputs:
     logits = torch.empty((B, L, V), dtype=torch.bfloat16, device=device)
@@ -297,17 +312,7 @@ def config5(device="cpu", V: int = V_LLADA, B: int = 1024, L: int = 32,
         if progress is not None and b0 % 256 == 0:
             progress(f"config5 inputs: sequences {b0}..{min(B, b0 + 256) - 1}")
         for b in range(b0, min(B, b0 + chunk)):
-            g = _gen(5, 0, b, device)
-            rows = _gumbel(g, (L, V), device)
-            tie = torch.rand((L,), generator=g, device=device) < 0.10
-            toks = _distinct_tokens(g, L, 2, V, device)
-            H = _uniform(g, (L, 1), 13.0, 17.0, device)
-            gap = _uniform(g, (L, 1), 0.0, 1e-3, device)
-            idx = torch.nonzero(tie).flatten()
-            if idx.numel():
-                pair = torch.cat([H[idx], H[idx] - gap[idx]], 1)
-                rows[idx] = rows[idx].scatter(1, toks[idx], pair)
-            logits[b] = rows.to(torch.bfloat16)
+            logits[b] = config5_rows(b, device, V, L)
     mask = torch.ones((B, L), dtype=torch.uint8, device=device)
     start = torch.zeros((B,), dtype=torch.int32, device=device)
     end = torch.full((B,), L, dtype=torch.int32, device=device)
