@@ -275,6 +275,29 @@ def per_config_report(fd, torch, workloads, dev, stream_gbps, reps):
         del gen
     gc.collect()
     torch.cuda.empty_cache()
+    # the same eight-sequence generation shape, run by the device-resident loop
+    # with the counter-based logits producer in place of the model call
+    loop_modes = [("graph, 8 steps per launch", 8, True),
+                  ("direct launches, 8 steps per host check", 8, False),
+                  ("direct launches, host check every step", 1, False)]
+    for V_loop, (mode, chunk, graph) in [(v, m) for v in (workloads.V_LLADA, 4096) for m in loop_modes]:
+        gen = fd.Generation(8, 256, 32, V_loop, 2026, "profile", 1.0, chunk=chunk,
+                            use_graph=graph, record_history=False, device=dev)
+        gen.run()                                    # warm-up
+        walls = []
+        for _ in range(5):
+            torch.cuda.synchronize()
+            t0 = time.perf_counter()
+            steps = gen.run()
+            walls.append(time.perf_counter() - t0)
+        w = sorted(walls)[len(walls) // 2]
+        rows.append({"config": "2-loop", "shape": f"B=8 gen 256 in blocks of 32, V={V_loop} bf16",
+                     "selector": "profile(1.0)", "mode": mode, "steps": steps,
+                     "ms_per_generation": 1e3 * w, "us_per_step": 1e6 * w / steps,
+                     "tokens_per_s": 8 * 256 / w})
+        log(f"device loop ({mode}): {steps} steps, {1e3 * w:.2f} ms per generation")
+        gen.close()
+        del gen
     log("per-config: config4 (first step of the generation)")
     gen = workloads.SimulatedGeneration(4, device=dev)
     inp = gen.prepare_step()
@@ -297,6 +320,8 @@ def per_config_markdown(rows, c5, stream_gbps, cmd) -> str:
            "| config | shape | selector | positions/step | kernel ms (cold) | kernel ms (hot) | "
            "positions/s | logits GB/s | % of 8 TB/s | % of stream | commits |",
            "|---|---|---|---|---|---|---|---|---|---|---|"]
+    loop = [r for r in rows if r["config"] == "2-loop"]
+    rows = [r for r in rows if r["config"] != "2-loop"]
     for r in rows + c5:
         hot = f"{r['kernel_ms_hot']:.4f}" if r["kernel_ms_hot"] is not None else "—"
         commits = (f"{r['commits_per_step']:.2f}/step, {r['steps']} steps" if "steps" in r
@@ -305,6 +330,15 @@ def per_config_markdown(rows, c5, stream_gbps, cmd) -> str:
         out.append(f"| {r['config']} | {r['shape']} | {r['selector']} | {r['positions_per_step']:.0f} | "
                    f"{r['kernel_ms_cold']:.4f} | {hot} | {r['positions_per_s']:.4g} | "
                    f"{r['logits_GBps']:.0f} | {100 * r['frac_of_peak']:.1f} | {fs} | {commits} |")
+    if loop:
+        out += ["", "Whole generations in the device-resident loop (`fdllm_generation_run`: "
+                "counter-based logits producer, decode step, block advance; wall clock of "
+                "`run()`, median of 5, the producer's time included):", "",
+                "| shape | mode | steps | ms per generation | µs per step | tokens/s |",
+                "|---|---|---|---|---|---|"]
+        for r in loop:
+            out.append(f"| {r['shape']} | {r['mode']} | {r['steps']} | {r['ms_per_generation']:.3f} | "
+                       f"{r['us_per_step']:.1f} | {r['tokens_per_s']:.4g} |")
     return "\n".join(out) + "\n"
 
 

@@ -187,6 +187,101 @@ fdllm_status fdllm_decode_step(const void* logits, fdllm_dtype dtype, int B, int
                                float* lse, uint8_t* commit, int32_t* n_commit, void* workspace,
                                size_t workspace_bytes, fdllm_stream stream);
 
+/*
+ * ---------------------------------------------------------------------------
+ * The decoding loop on the device (Alg. 1 outer loops)
+ * ---------------------------------------------------------------------------
+ * A generation of B sequences over a span of G positions in blocks of blk:
+ * every position starts masked, each sequence works on its first block that
+ * still has a masked position, and every step is a model call followed by
+ * fdllm_decode_step.  Here the model call is replaced by a synthetic,
+ * counter-based logits producer, so the whole loop runs without the host.
+ *
+ * Synthetic logits (bf16, row-major [B, G, V]).  Philox4x32-10 (Salmon,
+ * Moraes, Dror and Shaw, SC 2011) with key (seed mod 2^32, seed >> 32); for
+ * row (b, i) at step t and vocabulary index v:
+ *   background  w = philox(v >> 2, i, b, t)[v & 3]; (sum of w's 4 bytes - 510) * 2^-7
+ *   spike token philox(0xFFFFFFFF, i, b, 0xFFFFFFFF)[0] mod V (fixed over steps)
+ *   spike height y = philox(0xFFFFFFFE, i, b, t); u1 = (y[0] >> 8) 2^-24,
+ *               u2 = (y[1] >> 8) 2^-24; h = 8 + 6 u2 if u1 < 0.6 else 6 u2
+ *   logit       bf16(background + h) at the spike token, bf16(background)
+ *               elsewhere; float32 with every operation rounded to nearest,
+ *               bf16 by round-to-nearest-even.
+ * Only the rows of each sequence's active block are written.
+ */
+
+/*
+ * Writes the synthetic logits of the rows [block_start[b], block_end[b]) of
+ * every sequence b at step `step` (rows beyond blk slots of a window and
+ * rows outside it are untouched).
+ *   logits [B, L, V] bf16 (out); block_start, block_end [B] int32 (in);
+ *   blk: largest window (1..FDLLM_MAX_BLOCK).
+ */
+fdllm_status fdllm_synth_logits(void* logits, int B, int L, int V, int blk,
+                                const int32_t* block_start, const int32_t* block_end,
+                                uint64_t seed, int step, fdllm_stream stream);
+
+/*
+ * Block advance (Alg. 1: a block is decoded until none of its positions is
+ * masked, then the next block starts).  For every sequence, the window moves
+ * from its current block to the first block of blk positions at or after it
+ * that has a masked position; a sequence with none left gets [G, G).
+ *   mask [B, G] uint8 (in); block_start, block_end [B] int32 (in/out:
+ *   block_start must be a multiple of blk or G);
+ *   n_active [1] int32 (out, may be NULL): sequences left with a block.
+ */
+fdllm_status fdllm_advance_blocks(const uint8_t* mask, int32_t* block_start, int32_t* block_end,
+                                  int B, int G, int blk, int32_t* n_active, fdllm_stream stream);
+
+typedef struct {
+  int B, G, blk, V;          /* sequences, span, block size (<= FDLLM_MAX_BLOCK), vocabulary */
+  uint64_t seed;             /* synthetic logits generator seed */
+  fdllm_selector sel;        /* selector and its parameter (f, or tau), as fdllm_decode_step */
+  float param;
+  const float* eta;          /* robust rule: [B, G] allowances or NULL */
+  float eta_uniform;
+  int max_steps;             /* upper bound on steps; G always suffices */
+  int chunk;                 /* steps per launch; the host checks for completion between chunks */
+  int use_graph;             /* 1: capture `chunk` steps into a HIP graph and replay it;
+                                0: launch the kernels of each chunk directly */
+  void* logits;              /* [B, G, V] bf16 device buffer; active rows rewritten each step */
+  uint8_t* mask;             /* [B, G] out: final mask (all 0 when every block finished) */
+  int32_t* x;                /* [B, G] out: generated tokens (-1 where never revealed) */
+  int32_t* block_start;      /* [B] scratch/out: final windows */
+  int32_t* block_end;        /* [B] */
+  int32_t* n_commit_hist;    /* [max_steps, B] out (may be NULL): n_commit of every step */
+  void* workspace;           /* >= fdllm_generation_workspace_size() bytes of device memory */
+  size_t workspace_bytes;
+} fdllm_generation_desc;
+
+typedef struct fdllm_generation_s* fdllm_generation;
+
+/* Device workspace a generation needs (counters, n_commit, decode-step scratch). */
+fdllm_status fdllm_generation_workspace_size(const fdllm_generation_desc* desc, size_t* bytes);
+
+/*
+ * Prepares a generation: validates the description and, with use_graph,
+ * captures `chunk` steps (producer, decode step, advance, step counter) into
+ * a HIP graph.  All device memory is the caller's (the description's
+ * buffers); the object holds host-side runtime state only (a graph, a
+ * capture stream, two events and 64 bytes of pinned host memory).  The
+ * buffers must stay valid until fdllm_generation_destroy.
+ */
+fdllm_status fdllm_generation_create(const fdllm_generation_desc* desc, fdllm_generation* gen);
+
+/*
+ * Runs one whole generation on `stream`: resets mask = 1, x = -1, the
+ * windows to the first block and the counters, then launches chunks of
+ * steps until no sequence has a block left (read back once per chunk, one
+ * chunk behind the device) or max_steps is reached.  Blocks until the
+ * stream is idle; *steps (host, may be NULL) receives the number of steps
+ * in which some sequence still had a block (the NFE).  Runs of one object
+ * must not overlap.
+ */
+fdllm_status fdllm_generation_run(fdllm_generation gen, fdllm_stream stream, int32_t* steps);
+
+fdllm_status fdllm_generation_destroy(fdllm_generation gen);
+
 /* Workspace bytes fdllm_decode_step needs for these sizes (0 = none). */
 fdllm_status fdllm_workspace_size(int B, int L, int V, fdllm_dtype dtype, size_t* bytes);
 

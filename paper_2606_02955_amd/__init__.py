@@ -29,7 +29,21 @@ ERR_INVALID_ARG, ERR_UNSUPPORTED_DTYPE, ERR_SIZE, ERR_WORKSPACE, ERR_HIP = -1, -
 
 EXPORTS = ("fdllm_confidence", "fdllm_select_profile", "fdllm_select_factor",
            "fdllm_select_threshold", "fdllm_select_robust", "fdllm_reveal", "fdllm_decode_step",
-           "fdllm_workspace_size", "fdllm_status_string")
+           "fdllm_workspace_size", "fdllm_status_string", "fdllm_synth_logits",
+           "fdllm_advance_blocks", "fdllm_generation_workspace_size", "fdllm_generation_create",
+           "fdllm_generation_run", "fdllm_generation_destroy")
+
+
+class GenerationDesc(ctypes.Structure):
+    """fdllm_generation_desc (include/fdllm.h), field for field."""
+    _fields_ = [("B", ctypes.c_int), ("G", ctypes.c_int), ("blk", ctypes.c_int), ("V", ctypes.c_int),
+                ("seed", ctypes.c_uint64), ("sel", ctypes.c_int), ("param", ctypes.c_float),
+                ("eta", ctypes.c_void_p), ("eta_uniform", ctypes.c_float),
+                ("max_steps", ctypes.c_int), ("chunk", ctypes.c_int), ("use_graph", ctypes.c_int),
+                ("logits", ctypes.c_void_p), ("mask", ctypes.c_void_p), ("x", ctypes.c_void_p),
+                ("block_start", ctypes.c_void_p), ("block_end", ctypes.c_void_p),
+                ("n_commit_hist", ctypes.c_void_p), ("workspace", ctypes.c_void_p),
+                ("workspace_bytes", ctypes.c_size_t)]
 
 BENCH_EXPORTS = ("fdllm_stream_read",)
 
@@ -66,7 +80,16 @@ def load(path: Optional[str] = None) -> ctypes.CDLL:
     lib.fdllm_workspace_size.argtypes = [i32, i32, i32, i32, ctypes.POINTER(sz)]
     lib.fdllm_status_string.argtypes = [i32]
     lib.fdllm_status_string.restype = ctypes.c_char_p
-    for name in ("fdllm_confidence", "fdllm_reveal", "fdllm_decode_step", "fdllm_workspace_size"):
+    lib.fdllm_synth_logits.argtypes = [vp, i32, i32, i32, i32, vp, vp, ctypes.c_uint64, i32, vp]
+    lib.fdllm_advance_blocks.argtypes = [vp, vp, vp, i32, i32, i32, vp, vp]
+    dp = ctypes.POINTER(GenerationDesc)
+    lib.fdllm_generation_workspace_size.argtypes = [dp, ctypes.POINTER(sz)]
+    lib.fdllm_generation_create.argtypes = [dp, ctypes.POINTER(vp)]
+    lib.fdllm_generation_run.argtypes = [vp, vp, ctypes.POINTER(i32)]
+    lib.fdllm_generation_destroy.argtypes = [vp]
+    for name in ("fdllm_confidence", "fdllm_reveal", "fdllm_decode_step", "fdllm_workspace_size",
+                 "fdllm_synth_logits", "fdllm_advance_blocks", "fdllm_generation_workspace_size",
+                 "fdllm_generation_create", "fdllm_generation_run", "fdllm_generation_destroy"):
         getattr(lib, name).restype = i32
     if path is None:
         _lib = lib
@@ -200,6 +223,92 @@ def fdllm_decode_step(logits, mask, block_start, block_end, x, selector: str, pa
         ws_ptr, ws_bytes, _stream(logits.device))
     _check(st, "fdllm_decode_step")
     return workspace
+
+
+def fdllm_synth_logits(logits, block_start, block_end, blk: int, seed: int, step: int):
+    """Synthetic logits of every active block at `step` (recipe in fdllm.h)."""
+    B, L, V = logits.shape
+    if logits.dtype != torch.bfloat16:
+        raise ValueError("synthetic logits are bfloat16")
+    st = load().fdllm_synth_logits(
+        _ptr(logits, name="logits"), B, L, V, int(blk),
+        _ptr(block_start, torch.int32, (B,), "block_start"),
+        _ptr(block_end, torch.int32, (B,), "block_end"), int(seed) & ((1 << 64) - 1), int(step),
+        _stream(logits.device))
+    _check(st, "fdllm_synth_logits")
+
+
+def fdllm_advance_blocks(mask, block_start, block_end, blk: int, n_active=None):
+    """Move every window to its next block with a masked position (see fdllm.h)."""
+    B, G = mask.shape
+    st = load().fdllm_advance_blocks(
+        _ptr(mask, torch.uint8, (B, G), "mask"), _ptr(block_start, torch.int32, (B,), "block_start"),
+        _ptr(block_end, torch.int32, (B,), "block_end"), B, G, int(blk),
+        _ptr(n_active, torch.int32, (1,), "n_active"), _stream(mask.device))
+    _check(st, "fdllm_advance_blocks")
+
+
+class Generation:
+    """A device-resident generation (fdllm_generation_*): owns its torch buffers.
+
+    After run(): .x and .mask hold the result, .hist[t, b] the n_commit of
+    sequence b at step t (when record_history), and run() returns the steps.
+    """
+
+    def __init__(self, B: int, G: int, blk: int, V: int, seed: int, selector: str, param: float,
+                 eta=None, eta_uniform: float = 0.0, max_steps: Optional[int] = None,
+                 chunk: int = 8, use_graph: bool = True, record_history: bool = True,
+                 device=None):
+        if selector not in SELECTORS:
+            raise ValueError(f"selector must be one of {sorted(SELECTORS)}")
+        dev = torch.device(device) if device is not None else torch.device("cuda", torch.cuda.current_device())
+        self.lib = load()
+        self.device = dev
+        self.max_steps = int(max_steps or G)
+        self.logits = torch.empty((B, G, V), dtype=torch.bfloat16, device=dev)
+        self.mask = torch.empty((B, G), dtype=torch.uint8, device=dev)
+        self.x = torch.empty((B, G), dtype=torch.int32, device=dev)
+        self.start = torch.empty((B,), dtype=torch.int32, device=dev)
+        self.end = torch.empty((B,), dtype=torch.int32, device=dev)
+        self.hist = (torch.zeros((self.max_steps, B), dtype=torch.int32, device=dev)
+                     if record_history else None)
+        self.eta = eta
+        d = GenerationDesc()
+        d.B, d.G, d.blk, d.V = B, G, blk, V
+        d.seed, d.sel, d.param = int(seed) & ((1 << 64) - 1), SELECTORS[selector], float(param)
+        d.eta = _ptr(eta, torch.float32, (B, G), "eta")
+        d.eta_uniform = float(eta_uniform)
+        d.max_steps, d.chunk, d.use_graph = self.max_steps, int(chunk), int(bool(use_graph))
+        d.logits, d.mask, d.x = _ptr(self.logits), _ptr(self.mask), _ptr(self.x)
+        d.block_start, d.block_end = _ptr(self.start), _ptr(self.end)
+        d.n_commit_hist = _ptr(self.hist) if self.hist is not None else None
+        need = ctypes.c_size_t(0)
+        _check(self.lib.fdllm_generation_workspace_size(ctypes.byref(d), ctypes.byref(need)),
+               "fdllm_generation_workspace_size")
+        self.workspace = torch.empty(max(int(need.value), 1), dtype=torch.uint8, device=dev)
+        d.workspace, d.workspace_bytes = _ptr(self.workspace), int(need.value)
+        self.desc = d
+        h = ctypes.c_void_p(0)
+        _check(self.lib.fdllm_generation_create(ctypes.byref(d), ctypes.byref(h)),
+               "fdllm_generation_create")
+        self.handle = h
+
+    def run(self) -> int:
+        steps = ctypes.c_int32(0)
+        _check(self.lib.fdllm_generation_run(self.handle, _stream(self.device), ctypes.byref(steps)),
+               "fdllm_generation_run")
+        return int(steps.value)
+
+    def close(self):
+        if getattr(self, "handle", None) and self.handle.value:
+            self.lib.fdllm_generation_destroy(self.handle)
+            self.handle = ctypes.c_void_p(0)
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
 
 
 def select(selector: str, conf, eps, mask, block_start, block_end, param, commit, n_commit=None,

@@ -14,6 +14,7 @@ import sys
 PKG = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(PKG)
 SRC = os.path.join(PKG, "csrc", "fdllm.hip")
+LOOP_SRC = os.path.join(PKG, "csrc", "loop.hip")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(PKG, "libfdllm.so")
 BENCH_SRC = os.path.join(PKG, "csrc", "stream_read.hip")
@@ -41,23 +42,23 @@ def hipcc() -> str:
     raise RuntimeError("hipcc not found (ROCm is required to build libfdllm.so)")
 
 
-def _compile(src: str, lib: str, verbose: bool, extra=()) -> str:
+def _compile(srcs, lib: str, verbose: bool, extra=()) -> str:
     tmp = lib + ".tmp"
-    cmd = [hipcc(), *HIPCC_FLAGS, *extra, "-I", INCLUDE, src, "-o", tmp]
+    cmd = [hipcc(), *HIPCC_FLAGS, *extra, "-I", INCLUDE, *srcs, "-o", tmp]
     if verbose:
         print(" ".join(cmd), flush=True)
     res = subprocess.run(cmd, capture_output=True, text=True)
     if res.returncode != 0:
         sys.stderr.write(res.stdout + res.stderr)
-        raise RuntimeError(f"hipcc failed with status {res.returncode} on {src}")
+        raise RuntimeError(f"hipcc failed with status {res.returncode} on {srcs}")
     os.replace(tmp, lib)
     return lib
 
 
 def build(verbose: bool = False, extra=()) -> str:
     """Compile libfdllm.so and libfdllm_bench.so (always recompiles both)."""
-    _compile(BENCH_SRC, BENCH_LIB, verbose)
-    return _compile(SRC, LIB, verbose, extra)
+    _compile([BENCH_SRC], BENCH_LIB, verbose)
+    return _compile([SRC, LOOP_SRC], LIB, verbose, extra)
 
 
 if __name__ == "__main__":

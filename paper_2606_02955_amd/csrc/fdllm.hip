@@ -1004,7 +1004,6 @@ __global__ void __launch_bounds__(256) k_reveal(const uint8_t* __restrict__ comm
 struct Plan {
   bool fused;   // one workgroup per sequence, selection in the same kernel
   int split;    // wavefronts per row in the confidence kernel
-  int U;        // vectors per lane per batch
 };
 
 constexpr int kFusedMinB = 128;
@@ -1012,17 +1011,17 @@ constexpr int kFusedWaves = FDLLM_FUSED_WAVES;   // waves per workgroup in the f
 constexpr int kTargetWaves = FDLLM_TARGET_WAVES;   // row-streaming waves the split aims for
 
 static Plan make_plan(int B, int L, int V, fdllm_dtype dt) {
-  (void)V;
-  (void)dt;
   Plan p{};
   const long long win = L < kWaveBlock ? L : kWaveBlock;   // typical block: one wavefront
   p.fused = B >= kFusedMinB;
   p.split = 1;
   if (!p.fused) {
-    long long slots = (long long)B * win;
-    while (p.split < 16 && slots * p.split < kTargetWaves) p.split <<= 1;
+    // split rows while each part keeps at least 8 16-byte vectors per lane
+    const long long row_bytes = (long long)V * (dt == FDLLM_BF16 ? 2 : 4);
+    const long long max_split = row_bytes / (16LL * kWave * 8);
+    const long long slots = (long long)B * win;
+    while (p.split < 16 && 2LL * p.split <= max_split && slots * p.split < kTargetWaves) p.split <<= 1;
   }
-  p.U = 8;
   return p;
 }
 

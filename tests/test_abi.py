@@ -133,3 +133,55 @@ def test_bench_library_exports_and_checks(lib):
     assert blib.fdllm_stream_read(p, 32, None, None) == -1
     assert blib.fdllm_stream_read(p, 24, p, None) == -1              # not a multiple of 16
     assert blib.fdllm_stream_read(ctypes.c_void_p(0x1008), 32, p, None) == -1   # misaligned
+
+
+def test_generation_desc_layout_matches_header(tmp_path):
+    """The ctypes mirror of fdllm_generation_desc has the C compiler's layout."""
+    import shutil
+    import subprocess
+    if shutil.which("gcc") is None:
+        pytest.skip("gcc not available")
+    names = [f for f, _ in fd.GenerationDesc._fields_]
+    src = tmp_path / "layout.c"
+    src.write_text('#include <stdio.h>\n#include <stddef.h>\n#include "fdllm.h"\nint main(void) {\n'
+                   + f'  printf("%zu\\n", sizeof(fdllm_generation_desc));\n'
+                   + "".join(f'  printf("%zu\\n", offsetof(fdllm_generation_desc, {n}));\n' for n in names)
+                   + "  return 0;\n}\n")
+    exe = tmp_path / "layout"
+    subprocess.run(["gcc", "-std=c99", "-I", os.path.join(ROOT, "include"), str(src), "-o", str(exe)],
+                   check=True)
+    out = [int(v) for v in subprocess.run([str(exe)], capture_output=True, text=True,
+                                          check=True).stdout.split()]
+    assert out[0] == ctypes.sizeof(fd.GenerationDesc)
+    assert out[1:] == [getattr(fd.GenerationDesc, n).offset for n in names]
+
+
+def test_loop_entry_points_check_arguments(lib):
+    p = ctypes.c_void_p(0x1000)
+    null = None
+    assert lib.fdllm_synth_logits(null, 2, 8, 16, 4, p, p, 1, 0, null) == fd.ERR_INVALID_ARG
+    assert lib.fdllm_synth_logits(p, 2, 8, 16, 0, p, p, 1, 0, null) == fd.ERR_INVALID_ARG
+    assert lib.fdllm_synth_logits(p, 2, 8, 16, 2000, p, p, 1, 0, null) == fd.ERR_INVALID_ARG
+    assert lib.fdllm_synth_logits(p, 2, 8, 16, 4, p, p, 1, -1, null) == fd.ERR_INVALID_ARG
+    assert lib.fdllm_synth_logits(null, 0, 8, 16, 4, null, null, 1, 0, null) == 0
+    assert lib.fdllm_advance_blocks(null, p, p, 2, 8, 4, null, null) == fd.ERR_INVALID_ARG
+    assert lib.fdllm_advance_blocks(p, p, p, 2, 0, 4, null, null) == fd.ERR_INVALID_ARG
+    assert lib.fdllm_advance_blocks(null, null, null, 0, 8, 4, null, null) == 0
+    d = fd.GenerationDesc()
+    d.B, d.G, d.blk, d.V, d.seed, d.sel, d.param = 4, 64, 16, 100, 1, fd.SEL_PROFILE, 1.0
+    d.max_steps, d.chunk, d.use_graph = 64, 4, 1
+    n = ctypes.c_size_t(0)
+    assert lib.fdllm_generation_workspace_size(ctypes.byref(d), ctypes.byref(n)) == fd.ERR_INVALID_ARG
+    for f in ("logits", "mask", "x", "block_start", "block_end"):
+        setattr(d, f, 0x1000)
+    assert lib.fdllm_generation_workspace_size(ctypes.byref(d), ctypes.byref(n)) == 0
+    assert n.value >= 3 * 4 * 64 * 4                 # B=4 < 128: decode scratch included
+    h = ctypes.c_void_p(0)
+    assert lib.fdllm_generation_create(ctypes.byref(d), ctypes.byref(h)) == fd.ERR_WORKSPACE
+    assert not h.value
+    d.sel = 7
+    assert lib.fdllm_generation_create(ctypes.byref(d), ctypes.byref(h)) == fd.ERR_INVALID_ARG
+    d.sel, d.blk = fd.SEL_PROFILE, 2048
+    assert lib.fdllm_generation_workspace_size(ctypes.byref(d), ctypes.byref(n)) == fd.ERR_INVALID_ARG
+    assert lib.fdllm_generation_run(null, null, null) == fd.ERR_INVALID_ARG
+    assert lib.fdllm_generation_destroy(null) == 0
