@@ -189,6 +189,43 @@ fdllm_status fdllm_decode_step(const void* logits, fdllm_dtype dtype, int B, int
 
 /*
  * ---------------------------------------------------------------------------
+ * LM head fused with the vocabulary pass (Alg. 1: the model call's last
+ * layer followed by the per-position confidence)
+ * ---------------------------------------------------------------------------
+ * The logits of candidate position (b, i) are l_v = sum_k h[b,i,k] W[v,k],
+ * formed on the matrix cores with float32 accumulation (bf16 operands) and
+ * folded into the online (max, sum, argmax) of the vocabulary pass tile by
+ * tile; no logit is stored.  From the logits on, the outputs are those of
+ * fdllm_confidence (token, conf, eps, lse; defaults for non-candidates).
+ *   hidden [B, L, d] bf16, 16-byte aligned (in): final hidden states;
+ *   weight [V, d] bf16, 16-byte aligned (in): output embedding, row v for token v;
+ *   d: a multiple of 64 (FDLLM_ERR_SIZE otherwise);
+ *   mask, block_start, block_end: candidates as above;
+ *   workspace: at least fdllm_lmhead_workspace_size() bytes of device memory
+ *   (FDLLM_ERR_WORKSPACE otherwise), scratch between calls.
+ */
+fdllm_status fdllm_lmhead_workspace_size(int B, int L, int d, int V, size_t* bytes);
+fdllm_status fdllm_lmhead_confidence(const void* hidden, const void* weight, int B, int L, int d,
+                                     int V, const uint8_t* mask, const int32_t* block_start,
+                                     const int32_t* block_end, int32_t* tokens, float* conf,
+                                     float* eps, float* lse, void* workspace,
+                                     size_t workspace_bytes, fdllm_stream stream);
+
+/*
+ * One decoding step from hidden states: fdllm_lmhead_confidence, then the
+ * selector and the reveal as in fdllm_decode_step (same selector arguments;
+ * tokens, conf, eps, lse, commit, n_commit optional).
+ */
+fdllm_status fdllm_lmhead_decode_step(const void* hidden, const void* weight, int B, int L, int d,
+                                      int V, uint8_t* mask, const int32_t* block_start,
+                                      const int32_t* block_end, int32_t* x, fdllm_selector sel,
+                                      float param, const float* eta, float eta_uniform,
+                                      int32_t* tokens, float* conf, float* eps, float* lse,
+                                      uint8_t* commit, int32_t* n_commit, void* workspace,
+                                      size_t workspace_bytes, fdllm_stream stream);
+
+/*
+ * ---------------------------------------------------------------------------
  * The decoding loop on the device (Alg. 1 outer loops)
  * ---------------------------------------------------------------------------
  * A generation of B sequences over a span of G positions in blocks of blk:

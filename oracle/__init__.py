@@ -11,7 +11,9 @@ CPU restatement of what one decoding step of the paper's method computes:
     variant (appendix "Calibration-Robust Frechet Certificates"), by
     Fast-dLLM's factor rule and by the threshold rule (Sec. 2,
     "Confidence-Aware Parallel Decoding"; Sec. 5, "Baselines");
-  * the reveal of the chosen tokens (Alg. 1, reveal step).
+  * the reveal of the chosen tokens (Alg. 1, reveal step);
+  * for the LM-head form, the logits as float64 dot products of hidden
+    states with the output embedding (``lmhead``).
 
 It shares no code with the HIP library and imports nothing from it.  Only the
 tests, ``__graft_entry__.smoke()`` and the ``cpu_baseline`` leg of
@@ -32,9 +34,11 @@ from .rules import (sorted_order, factor_n_star, profile_n_star, profile_literal
                      profile_adaptive_n_star, threshold_set, select_block, select, SelectResult,
                      frechet_quantities, robust_eps, FLAG_WINDOW)
 from .step import decode_step, StepResult
+from . import lmhead
 
 __all__ = [
     "position_confidence", "confidence", "sorted_order", "factor_n_star", "profile_n_star",
     "profile_literal_n_star", "profile_adaptive_n_star", "threshold_set", "select_block",
     "select", "SelectResult", "frechet_quantities", "robust_eps", "FLAG_WINDOW", "decode_step", "StepResult",
+    "lmhead",
 ]

@@ -31,7 +31,8 @@ EXPORTS = ("fdllm_confidence", "fdllm_select_profile", "fdllm_select_factor",
            "fdllm_select_threshold", "fdllm_select_robust", "fdllm_reveal", "fdllm_decode_step",
            "fdllm_workspace_size", "fdllm_status_string", "fdllm_synth_logits",
            "fdllm_advance_blocks", "fdllm_generation_workspace_size", "fdllm_generation_create",
-           "fdllm_generation_run", "fdllm_generation_destroy")
+           "fdllm_generation_run", "fdllm_generation_destroy", "fdllm_lmhead_workspace_size",
+           "fdllm_lmhead_confidence", "fdllm_lmhead_decode_step")
 
 
 class GenerationDesc(ctypes.Structure):
@@ -80,6 +81,11 @@ def load(path: Optional[str] = None) -> ctypes.CDLL:
     lib.fdllm_workspace_size.argtypes = [i32, i32, i32, i32, ctypes.POINTER(sz)]
     lib.fdllm_status_string.argtypes = [i32]
     lib.fdllm_status_string.restype = ctypes.c_char_p
+    lib.fdllm_lmhead_workspace_size.argtypes = [i32, i32, i32, i32, ctypes.POINTER(sz)]
+    lib.fdllm_lmhead_confidence.argtypes = [vp, vp, i32, i32, i32, i32, vp, vp, vp, vp, vp, vp, vp,
+                                            vp, sz, vp]
+    lib.fdllm_lmhead_decode_step.argtypes = [vp, vp, i32, i32, i32, i32, vp, vp, vp, vp, i32, f32,
+                                             vp, f32, vp, vp, vp, vp, vp, vp, vp, sz, vp]
     lib.fdllm_synth_logits.argtypes = [vp, i32, i32, i32, i32, vp, vp, ctypes.c_uint64, i32, vp]
     lib.fdllm_advance_blocks.argtypes = [vp, vp, vp, i32, i32, i32, vp, vp]
     dp = ctypes.POINTER(GenerationDesc)
@@ -89,6 +95,7 @@ def load(path: Optional[str] = None) -> ctypes.CDLL:
     lib.fdllm_generation_destroy.argtypes = [vp]
     for name in ("fdllm_confidence", "fdllm_reveal", "fdllm_decode_step", "fdllm_workspace_size",
                  "fdllm_synth_logits", "fdllm_advance_blocks", "fdllm_generation_workspace_size",
+                 "fdllm_lmhead_workspace_size", "fdllm_lmhead_confidence", "fdllm_lmhead_decode_step",
                  "fdllm_generation_create", "fdllm_generation_run", "fdllm_generation_destroy"):
         getattr(lib, name).restype = i32
     if path is None:
@@ -222,6 +229,64 @@ def fdllm_decode_step(logits, mask, block_start, block_end, x, selector: str, pa
         _ptr(commit, torch.uint8, (B, L), "commit"), _ptr(n_commit, torch.int32, (B,), "n_commit"),
         ws_ptr, ws_bytes, _stream(logits.device))
     _check(st, "fdllm_decode_step")
+    return workspace
+
+
+def fdllm_lmhead_workspace_size(B: int, L: int, d: int, V: int) -> int:
+    n = ctypes.c_size_t(0)
+    _check(load().fdllm_lmhead_workspace_size(B, L, d, V, ctypes.byref(n)), "fdllm_lmhead_workspace_size")
+    return int(n.value)
+
+
+def _lm_args(hidden, weight):
+    B, L, d = hidden.shape
+    V, d2 = weight.shape
+    if d2 != d:
+        raise ValueError(f"weight must be [V, {d}], got {tuple(weight.shape)}")
+    if hidden.dtype != torch.bfloat16 or weight.dtype != torch.bfloat16:
+        raise ValueError("hidden and weight must be bfloat16")
+    return B, L, d, V
+
+
+def _lm_workspace(workspace, B, L, d, V, device):
+    if workspace is None:
+        workspace = torch.empty(fdllm_lmhead_workspace_size(B, L, d, V), dtype=torch.uint8, device=device)
+    return workspace, _ptr(workspace, name="workspace"), workspace.numel() * workspace.element_size()
+
+
+def fdllm_lmhead_confidence(hidden, weight, mask, block_start, block_end, tokens, conf, eps=None,
+                            lse=None, workspace=None):
+    """Greedy token / confidence / eps / lse from hidden states (see fdllm.h)."""
+    B, L, d, V = _lm_args(hidden, weight)
+    workspace, wp, wb = _lm_workspace(workspace, B, L, d, V, hidden.device)
+    st = load().fdllm_lmhead_confidence(
+        _ptr(hidden, name="hidden"), _ptr(weight, name="weight"), B, L, d, V,
+        _ptr(mask, torch.uint8, (B, L), "mask"), _ptr(block_start, torch.int32, (B,), "block_start"),
+        _ptr(block_end, torch.int32, (B,), "block_end"), _ptr(tokens, torch.int32, (B, L), "tokens"),
+        _ptr(conf, torch.float32, (B, L), "conf"), _ptr(eps, torch.float32, (B, L), "eps"),
+        _ptr(lse, torch.float32, (B, L), "lse"), wp, wb, _stream(hidden.device))
+    _check(st, "fdllm_lmhead_confidence")
+    return workspace
+
+
+def fdllm_lmhead_decode_step(hidden, weight, mask, block_start, block_end, x, selector: str,
+                             param: float, tokens=None, conf=None, eps=None, lse=None, commit=None,
+                             n_commit=None, workspace=None, eta=None, eta_uniform: float = 0.0):
+    """One decoding step from hidden states; mask and x updated in place (see fdllm.h)."""
+    B, L, d, V = _lm_args(hidden, weight)
+    if selector not in SELECTORS:
+        raise ValueError(f"selector must be one of {sorted(SELECTORS)}")
+    workspace, wp, wb = _lm_workspace(workspace, B, L, d, V, hidden.device)
+    st = load().fdllm_lmhead_decode_step(
+        _ptr(hidden, name="hidden"), _ptr(weight, name="weight"), B, L, d, V,
+        _ptr(mask, torch.uint8, (B, L), "mask"), _ptr(block_start, torch.int32, (B,), "block_start"),
+        _ptr(block_end, torch.int32, (B,), "block_end"), _ptr(x, torch.int32, (B, L), "x"),
+        SELECTORS[selector], float(param), _ptr(eta, torch.float32, (B, L), "eta"), float(eta_uniform),
+        _ptr(tokens, torch.int32, (B, L), "tokens"), _ptr(conf, torch.float32, (B, L), "conf"),
+        _ptr(eps, torch.float32, (B, L), "eps"), _ptr(lse, torch.float32, (B, L), "lse"),
+        _ptr(commit, torch.uint8, (B, L), "commit"), _ptr(n_commit, torch.int32, (B,), "n_commit"),
+        wp, wb, _stream(hidden.device))
+    _check(st, "fdllm_lmhead_decode_step")
     return workspace
 
 

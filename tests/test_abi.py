@@ -185,3 +185,32 @@ def test_loop_entry_points_check_arguments(lib):
     assert lib.fdllm_generation_workspace_size(ctypes.byref(d), ctypes.byref(n)) == fd.ERR_INVALID_ARG
     assert lib.fdllm_generation_run(null, null, null) == fd.ERR_INVALID_ARG
     assert lib.fdllm_generation_destroy(null) == 0
+
+
+def test_lmhead_entry_points_check_arguments(lib):
+    p = ctypes.c_void_p(0x1000)
+    null = None
+    n = ctypes.c_size_t(0)
+    assert lib.fdllm_lmhead_workspace_size(4, 32, 4096, 126464, ctypes.byref(n)) == 0
+    assert n.value >= 4 * 32 * 4                     # row list at least
+    assert lib.fdllm_lmhead_workspace_size(4, 32, 100, 1000, ctypes.byref(n)) == fd.ERR_SIZE   # d % 64
+    assert lib.fdllm_lmhead_workspace_size(4, 32, 0, 1000, ctypes.byref(n)) == fd.ERR_SIZE
+    assert lib.fdllm_lmhead_workspace_size(4, 32, 64, 0, ctypes.byref(n)) == fd.ERR_SIZE
+    assert lib.fdllm_lmhead_workspace_size(4, 32, 64, 10, None) == fd.ERR_INVALID_ARG
+    args = lambda **kw: [kw.get("h", p), kw.get("w", p), 2, 8, kw.get("d", 64), 100, kw.get("m", p), p, p,
+                         kw.get("tok", p), kw.get("conf", p), null, null, kw.get("ws", p),
+                         kw.get("wsb", 1 << 30), null]
+    assert lib.fdllm_lmhead_confidence(*args(h=null)) == fd.ERR_INVALID_ARG
+    assert lib.fdllm_lmhead_confidence(*args(w=null)) == fd.ERR_INVALID_ARG
+    assert lib.fdllm_lmhead_confidence(*args(m=null)) == fd.ERR_INVALID_ARG
+    assert lib.fdllm_lmhead_confidence(*args(tok=null)) == fd.ERR_INVALID_ARG
+    assert lib.fdllm_lmhead_confidence(*args(d=96)) == fd.ERR_SIZE
+    assert lib.fdllm_lmhead_confidence(*args(h=ctypes.c_void_p(0x1008))) == fd.ERR_INVALID_ARG  # alignment
+    assert lib.fdllm_lmhead_confidence(*args(ws=null, wsb=0)) == fd.ERR_WORKSPACE
+    assert lib.fdllm_lmhead_confidence(*args(wsb=64)) == fd.ERR_WORKSPACE
+    dargs = [p, p, 2, 8, 64, 100, p, p, p, p, 9, 1.0, null, 0.0, null, null, null, null, null, null,
+             p, 1 << 30, null]
+    assert lib.fdllm_lmhead_decode_step(*dargs) == fd.ERR_INVALID_ARG          # selector 9
+    dargs[10] = 2
+    dargs[9] = None
+    assert lib.fdllm_lmhead_decode_step(*dargs) == fd.ERR_INVALID_ARG          # x missing

@@ -380,3 +380,58 @@ CONFIGS = {
     5: dict(B=1024, L=32, V=V_LLADA, dtype="bf16", selectors=["profile", "factor", "threshold"],
             params=dict(profile=[1.0, 0.75], factor=[1.0, 0.75], threshold=[0.9])),
 }
+
+
+# ---------------------------------------------------------------------------
+# LM-head inputs: hidden states [B, L, d] and an output embedding [V, d], both
+# bf16, for the fused LM head + vocabulary pass.  Two recipes:
+#   exact:  W entries in {-3..3}/4; a candidate row aimed at token t has
+#           h = (s * W[t] + 4 r) / 4 * 2^(q-7) with r in {-3..3}/4, a per-row
+#           strength s in {0..16} and q = round(log2(4096/d)).  Up to the
+#           power of two, every product is a multiple of 2^-11 and every
+#           partial sum stays below 2^20 of those units, so the logits are
+#           exact in float32 whatever the order of accumulation.  Some rows
+#           aim at token pairs with identical W rows (exact ties).
+#   random: W ~ N(0, 1/d), h = a W[t] / |W[t]|^2 + N(0, 1) with a ~ U(0, 24)
+#           (a spike of height a over a unit-variance background), general
+#           bf16 values (results compared within rounding bounds).
+# ---------------------------------------------------------------------------
+def lmhead_case(B: int, L: int, d: int, V: int, kind: str = "exact", device="cpu", seed: int = 0,
+                window: Optional[int] = None, p_mask: float = 0.8, tie_pairs: int = 4):
+    g = torch.Generator(device="cpu")
+    g.manual_seed(seed_for(200 + seed % 1000, seed // 1000, 0))
+    window = min(L, 64) if window is None else window
+    lens = torch.randint(0, window + 1, (B,), generator=g)
+    start = torch.tensor([int(torch.randint(0, L - int(lens[b]) + 1, (1,), generator=g)) for b in range(B)],
+                         dtype=torch.int32)
+    end = start + lens.to(torch.int32)
+    mask = (torch.rand((B, L), generator=g) < p_mask).to(torch.uint8)
+    target = torch.randint(0, V, (B, L), generator=g)
+    if kind == "exact":
+        w = torch.randint(-3, 4, (V, d), generator=g).float() / 4
+        # tie pairs: W[t2] = W[t1], some rows aimed at t1 or t2
+        pairs = torch.randint(0, V, (tie_pairs, 2), generator=g)
+        for t1, t2 in pairs.tolist():
+            if t1 != t2:
+                w[max(t1, t2)] = w[min(t1, t2)]
+        flat = target.view(-1)
+        aim = torch.rand(flat.shape, generator=g) < 0.1
+        flat[aim] = pairs[torch.randint(0, tie_pairs, (int(aim.sum()),), generator=g),
+                          torch.randint(0, 2, (int(aim.sum()),), generator=g)]
+        s = torch.randint(0, 17, (B, L, 1), generator=g).float()
+        r = torch.randint(-3, 4, (B, L, d), generator=g).float() / 4
+        # a power of two keeps every value exact and the spike's logit near 2 s for any d
+        scale = 2.0 ** (round(math.log2(4096 / d)) - 7)
+        h = (s * w[target] + 4 * r) / 4 * scale
+    elif kind == "random":
+        w = torch.randn((V, d), generator=g) / math.sqrt(d)
+        a = torch.rand((B, L, 1), generator=g) * 24.0
+        wt = w[target]
+        h = a * wt / (wt * wt).sum(-1, keepdim=True) + torch.randn((B, L, d), generator=g)
+    else:
+        raise ValueError(f"unknown LM-head recipe {kind!r}")
+    hidden = h.to(torch.bfloat16).to(device)
+    weight = w.to(torch.bfloat16).to(device)
+    x = torch.full((B, L), MASK_ID, dtype=torch.int32)
+    return (hidden, weight, mask.to(device), start.to(device), end.to(device), x.to(device),
+            f"lmhead-{kind}(B={B},L={L},d={d},V={V},seed={seed})")
