@@ -18,8 +18,8 @@ read-only stream of the same logits buffer (libfdllm_bench.so).
 on all host cores (one process per core, each on its own sequences) and on
 one core.  `--per-config` adds the other workload recipes (one sequence fp32;
 eight-sequence and 256-sequence simulated generations; 64 sequences in a
-512-position span), cold and cache-hot, and can write them as a markdown
-table.
+512-position span), cold and cache-hot, the device-resident generation loop
+and the LM head fused with the pass, and can write them as a markdown table.
 """
 from __future__ import annotations
 
@@ -298,6 +298,51 @@ def per_config_report(fd, torch, workloads, dev, stream_gbps, reps):
         log(f"device loop ({mode}): {steps} steps, {1e3 * w:.2f} ms per generation")
         gen.close()
         del gen
+    # LM head fused with the vocabulary pass (hidden states in, no logits in HBM)
+    # against the unfused pair: a hipBLASLt GEMM writing bf16 logits, then the pass
+    d_model = 4096
+    gw = torch.Generator(device=dev).manual_seed(2606)
+    weight = (torch.randn((workloads.V_LLADA, d_model), generator=gw, device=dev) / 64).to(torch.bfloat16)
+    for B_lm in (8, 128):
+        L_lm = 32
+        hid = torch.randn((B_lm, L_lm, d_model), generator=gw, device=dev).to(torch.bfloat16)
+        mk = torch.ones((B_lm, L_lm), dtype=torch.uint8, device=dev)
+        st_ = torch.zeros(B_lm, dtype=torch.int32, device=dev)
+        en_ = torch.full((B_lm,), L_lm, dtype=torch.int32, device=dev)
+        tok = torch.empty((B_lm, L_lm), dtype=torch.int32, device=dev)
+        cf = torch.empty((B_lm, L_lm), device=dev)
+        ws = fd.fdllm_lmhead_confidence(hid, weight, mk, st_, en_, tok, cf)
+        lg = torch.empty((B_lm * L_lm, workloads.V_LLADA), dtype=torch.bfloat16, device=dev)
+        torch.matmul(hid.view(-1, d_model), weight.t(), out=lg)
+        torch.cuda.synchronize()
+        tf, tg, tp = [], [], []
+        for _ in range(max(3, reps // 2)):
+            e0, e1, e2, e3 = (torch.cuda.Event(enable_timing=True) for _ in range(4))
+            e0.record()
+            fd.fdllm_lmhead_confidence(hid, weight, mk, st_, en_, tok, cf, workspace=ws)
+            e1.record()
+            torch.matmul(hid.view(-1, d_model), weight.t(), out=lg)
+            e2.record()
+            fd.fdllm_confidence(lg.view(B_lm, L_lm, -1), mk, st_, en_, tok, cf)
+            e3.record()
+            torch.cuda.synchronize()
+            tf.append(e0.elapsed_time(e1) * 1e-3)
+            tg.append(e1.elapsed_time(e2) * 1e-3)
+            tp.append(e2.elapsed_time(e3) * 1e-3)
+        med = lambda v: sorted(v)[len(v) // 2]
+        flops = 2.0 * B_lm * L_lm * d_model * workloads.V_LLADA
+        rows.append({"config": "lmhead", "shape": f"{B_lm * L_lm} positions, d={d_model}, V={workloads.V_LLADA}",
+                     "fused_ms": 1e3 * med(tf), "fused_TFLOPs": flops / med(tf) / 1e12,
+                     "frac_of_bf16_peak": flops / med(tf) / 2.5e15,
+                     "unfused_gemm_ms": 1e3 * med(tg), "unfused_pass_ms": 1e3 * med(tp),
+                     "unfused_TFLOPs": flops / (med(tg) + med(tp)) / 1e12,
+                     "logits_bytes_avoided": B_lm * L_lm * workloads.V_LLADA * 2})
+        log(f"lmhead {B_lm * L_lm} positions: fused {1e3 * med(tf):.3f} ms, "
+            f"hipBLASLt {1e3 * med(tg):.3f} ms + pass {1e3 * med(tp):.3f} ms")
+        del hid, lg, ws
+    del weight
+    gc.collect()
+    torch.cuda.empty_cache()
     log("per-config: config4 (first step of the generation)")
     gen = workloads.SimulatedGeneration(4, device=dev)
     inp = gen.prepare_step()
@@ -321,7 +366,8 @@ def per_config_markdown(rows, c5, stream_gbps, cmd) -> str:
            "positions/s | logits GB/s | % of 8 TB/s | % of stream | commits |",
            "|---|---|---|---|---|---|---|---|---|---|---|"]
     loop = [r for r in rows if r["config"] == "2-loop"]
-    rows = [r for r in rows if r["config"] != "2-loop"]
+    lm = [r for r in rows if r["config"] == "lmhead"]
+    rows = [r for r in rows if r["config"] not in ("2-loop", "lmhead")]
     for r in rows + c5:
         hot = f"{r['kernel_ms_hot']:.4f}" if r["kernel_ms_hot"] is not None else "—"
         commits = (f"{r['commits_per_step']:.2f}/step, {r['steps']} steps" if "steps" in r
@@ -339,6 +385,18 @@ def per_config_markdown(rows, c5, stream_gbps, cmd) -> str:
         for r in loop:
             out.append(f"| {r['shape']} | {r['mode']} | {r['steps']} | {r['ms_per_generation']:.3f} | "
                        f"{r['us_per_step']:.1f} | {r['tokens_per_s']:.4g} |")
+    if lm:
+        out += ["", "LM head fused with the vocabulary pass (`fdllm_lmhead_confidence`: bf16 hidden "
+                "states x bf16 output embedding on the matrix cores, online softmax in the epilogue, no "
+                "logits stored) against the unfused pair (hipBLASLt GEMM to bf16 logits via torch.matmul, "
+                "then `fdllm_confidence`); HIP-event medians:", "",
+                "| shape | fused ms | fused TFLOP/s | % of 2.5 PFLOP/s | GEMM ms | pass ms | unfused TFLOP/s | logits not stored |",
+                "|---|---|---|---|---|---|---|---|"]
+        for r in lm:
+            out.append(f"| {r['shape']} | {r['fused_ms']:.3f} | {r['fused_TFLOPs']:.0f} | "
+                       f"{100 * r['frac_of_bf16_peak']:.1f} | {r['unfused_gemm_ms']:.3f} | "
+                       f"{r['unfused_pass_ms']:.3f} | {r['unfused_TFLOPs']:.0f} | "
+                       f"{r['logits_bytes_avoided'] / 1e6:.0f} MB |")
     return "\n".join(out) + "\n"
 
 

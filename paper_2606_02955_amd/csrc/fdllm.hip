@@ -1249,23 +1249,31 @@ k_lm_partial(const uint16_t* __restrict__ hidden, const uint16_t* __restrict__ w
 
 constexpr size_t kLmLdsBytes = (size_t)(2 * kLmVt + 2 * kLmPt) * kLmRowVec * sizeof(u32x4);
 
-// Per candidate row: combine the splits' partials in split order, finish.
+// Per candidate row, one wavefront: lane l combines the splits l, l+64, ...
+// of the row's contiguous partials, then a fixed butterfly over the lanes
+// (both partners of every step form the same sum) and the finish.
 __global__ void __launch_bounds__(256)
 k_lm_finish(const int32_t* __restrict__ rows, const int32_t* __restrict__ count,
             const WavePartial* __restrict__ partials, int n_split, RowOut out) {
-  const int k = blockIdx.x * blockDim.x + threadIdx.x;
+  const int lane = threadIdx.x % kWave;
+  const int k = blockIdx.x * 4 + threadIdx.x / kWave;
   if (k >= *count) return;
   const WavePartial* p = partials + (size_t)k * n_split;
-  float M = p[0].m;
-  for (int j = 1; j < n_split; ++j) M = fmaxf(M, p[j].m);
+  float M = kNegInf;
+  for (int j = lane; j < n_split; j += kWave) M = fmaxf(M, p[j].m);
+  M = wave_max(M);
   const float K = exp_ref(M);
   double S = 0.0;
   int first = 0x7fffffff;
-  for (int j = 0; j < n_split; ++j) {
-    S += rescale(p[j].S, p[j].K, K);
-    if (p[j].m == M) first = min(first, p[j].first);
+  for (int j = lane; j < n_split; j += kWave) {
+    const WavePartial q = p[j];
+    S += rescale(q.S, q.K, K);
+    if (q.m == M) first = min(first, q.first);
   }
-  store_row(out, (size_t)rows[k], finish_row(M, K, S, first));
+#pragma unroll
+  for (int d = kWave / 2; d >= 1; d >>= 1) S += __shfl_xor(S, d);
+  first = wave_min(first);
+  if (lane == 0) store_row(out, (size_t)rows[k], finish_row(M, K, S, first));
 }
 
 // ---------------------------------------------------------------------------
@@ -1494,7 +1502,7 @@ static hipError_t lm_launch(const void* hidden, const void* weight, int B, int L
                      kLmLdsBytes, st, (const uint16_t*)hidden, (const uint16_t*)weight, rows, count,
                      d, V, p.tiles_per_split, part, p.n_split);
   const long long n = (long long)B * L;
-  hipLaunchKernelGGL(k_lm_finish, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, st, rows, count,
+  hipLaunchKernelGGL(k_lm_finish, dim3((unsigned)((n + 3) / 4)), dim3(256), 0, st, rows, count,
                      part, p.n_split, out);
   return hipGetLastError();
 }
