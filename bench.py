@@ -37,7 +37,8 @@ sys.path.insert(0, ROOT)
 METRIC = "masked positions selected/sec + logits-read HBM GB/s (% of peak), 1 GPU"
 HBM_PEAK_GBPS = 8000.0
 IO_BYTES_PER_POSITION = 18   # mask read, commit, tokens, conf, eps, lse (1+1+4+4+4+4)
-SRC = os.path.join(ROOT, "paper_2606_02955_amd", "csrc", "fdllm.hip")
+# sources of the vocabulary pass kernels (the fused decode step and its helpers)
+SRCS = [os.path.join(ROOT, "paper_2606_02955_amd", "csrc", f) for f in ("fdllm.hip", "pass_common.h")]
 TRAFFIC = os.path.join(ROOT, "profiles", "traffic_fused_decode_config5.json")
 MAX_HOST_WORKERS = 16        # host CPU share of one GPU
 
@@ -47,7 +48,10 @@ def log(msg: str):
 
 
 def source_digest() -> str:
-    return hashlib.sha256(open(SRC, "rb").read()).hexdigest()[:16]
+    h = hashlib.sha256()
+    for f in SRCS:
+        h.update(open(f, "rb").read())
+    return h.hexdigest()[:16]
 
 
 def measured_traffic():

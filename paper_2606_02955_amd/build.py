@@ -15,6 +15,7 @@ PKG = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(PKG)
 SRC = os.path.join(PKG, "csrc", "fdllm.hip")
 LOOP_SRC = os.path.join(PKG, "csrc", "loop.hip")
+LMHEAD_SRC = os.path.join(PKG, "csrc", "lmhead.hip")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(PKG, "libfdllm.so")
 BENCH_SRC = os.path.join(PKG, "csrc", "stream_read.hip")
@@ -58,7 +59,7 @@ def _compile(srcs, lib: str, verbose: bool, extra=()) -> str:
 def build(verbose: bool = False, extra=()) -> str:
     """Compile libfdllm.so and libfdllm_bench.so (always recompiles both)."""
     _compile([BENCH_SRC], BENCH_LIB, verbose)
-    return _compile([SRC, LOOP_SRC], LIB, verbose, extra)
+    return _compile([SRC, LMHEAD_SRC, LOOP_SRC], LIB, verbose, extra)
 
 
 if __name__ == "__main__":
