@@ -199,7 +199,8 @@ fdllm_status fdllm_decode_step(const void* logits, fdllm_dtype dtype, int B, int
  * fdllm_confidence (token, conf, eps, lse; defaults for non-candidates).
  *   hidden [B, L, d] bf16, 16-byte aligned (in): final hidden states;
  *   weight [V, d] bf16, 16-byte aligned (in): output embedding, row v for token v;
- *   d: a multiple of 64 (FDLLM_ERR_SIZE otherwise);
+ *   d: a multiple of 64, hidden at most 4 GiB (B*L*d*2 < 2^32 bytes) and
+ *   V*d/8 < 2^31 (FDLLM_ERR_SIZE otherwise);
  *   mask, block_start, block_end: candidates as above;
  *   workspace: at least fdllm_lmhead_workspace_size() bytes of device memory
  *   (FDLLM_ERR_WORKSPACE otherwise), scratch between calls.

@@ -30,8 +30,10 @@ HIPCC_FLAGS = [
     "-shared",
     # packed-FP32 VALU forms stay disabled on this target
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
-    # logits are finite by contract: max/min need no NaN quieting
-    "-Xarch_device", "-fno-honor-nans", "-Xarch_device", "-mno-amdgpu-ieee",
+    # logits are finite by contract: max/min need no NaN quieting.  (Not
+    # -mno-amdgpu-ieee: the device library keeps IEEE mode, and its work-item
+    # and workgroup id functions would then stay out-of-line calls.)
+    "-Xarch_device", "-fno-honor-nans",
     "-Wno-unused-command-line-argument",
 ]
 

@@ -2,14 +2,24 @@
 //
 // Alg. 1's model call ends in the output projection: a candidate position's
 // logits are l_v = sum_k h_k W_vk.  Here they are formed tile by tile on the
-// matrix cores (v_mfma_f32_32x32x16_bf16, bf16 operands, float32
+// matrix cores (v_mfma_f32_16x16x32_bf16, bf16 operands, float32
 // accumulation) and folded straight into the vocabulary pass's online
 // (maximum, exponent reference, sum, argmax) state, so no logit reaches HBM;
 // the per-position outputs and the selection are then those of
 // fdllm_confidence / fdllm_decode_step (Sec. 3 "Notation"; Alg. 1).
+//
+// Main loop of the partial kernel: a workgroup of 8 waves owns 256 candidate
+// positions x 256 vocabulary rows per tile; the hidden dimension streams in
+// stages of 32 elements (32 KiB of weight and hidden rows per stage) that
+// buffer_load ... lds writes straight into LDS, four stages resident so the
+// loads of a stage go out three stages before it is used.  One barrier per
+// stage; each wave's 32 MFMAs of a stage are interleaved with the reads of
+// the next stage's operands and with the stage loads.
 #include <hip/hip_runtime.h>
 
 #include <stdint.h>
+
+#include <atomic>
 
 #include "fdllm.h"
 #include "pass_common.h"
@@ -22,16 +32,14 @@ namespace fdllm {
 // (max, exponent reference, sum, argmax) state; no logit is written to HBM.
 // ---------------------------------------------------------------------------
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
-typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
 
 constexpr int kLmWaves = 8;                    // waves per workgroup
 constexpr int kLmVt = 256;                     // vocabulary rows per tile (MFMA A operand)
 constexpr int kLmPt = 256;                     // positions per workgroup (MFMA B operand)
-constexpr int kLmBK = 64;                      // hidden-dimension elements per LDS stage
-constexpr int kLmRowVec = kLmBK / 8 + 1;       // 16-byte vectors per LDS row (one of padding)
+constexpr int kLmBK = 32;                      // hidden-dimension elements per LDS stage
+constexpr int kLmNBuf = 4;                     // stages resident in LDS
 constexpr int kLmThreads = kLmWaves * kWave;
-constexpr int kLmWChunks = kLmVt * (kLmBK / 8) / kLmThreads;   // 16-byte loads per thread
-constexpr int kLmHChunks = kLmPt * (kLmBK / 8) / kLmThreads;
 constexpr int kLmRows = kLmPt;                 // candidate rows per workgroup
 constexpr int kLmCols = kLmVt;                 // vocabulary columns per tile
 
@@ -73,16 +81,16 @@ struct LmState {
   int first;
 };
 
-// Folds the lane's 64 accumulators of one position (vocabulary entries
-// base + 32 mi + 8 (i/4) + 4 h + i%4, increasing in (mi, i)) into its state.
-__device__ __forceinline__ void lm_fold(LmState& st, const f32x16 (&acc)[4][2], int ni, int base,
-                                        int V) {
+// Folds the lane's 32 accumulators of one position (vocabulary entries
+// base + 16 mi + i, increasing in (mi, i)) into its state.
+__device__ __forceinline__ void lm_fold(LmState& st, const f32x4 (&acc)[8][4], int ni, int base,
+                                          int V) {
   float tm = kNegInf;
 #pragma unroll
-  for (int mi = 0; mi < 4; ++mi)
+  for (int mi = 0; mi < 8; ++mi)
 #pragma unroll
-    for (int i = 0; i < 16; ++i) {
-      const int v = base + 32 * mi + 8 * (i / 4) + i % 4;
+    for (int i = 0; i < 4; ++i) {
+      const int v = base + 16 * mi + i;
       if (v < V) tm = fmaxf(tm, acc[mi][ni][i]);
     }
   if (tm > st.M) {
@@ -92,10 +100,10 @@ __device__ __forceinline__ void lm_fold(LmState& st, const f32x16 (&acc)[4][2], 
     st.M = tm;
     int f = 0x7fffffff;
 #pragma unroll
-    for (int mi = 3; mi >= 0; --mi)
+    for (int mi = 7; mi >= 0; --mi)
 #pragma unroll
-      for (int i = 15; i >= 0; --i) {
-        const int v = base + 32 * mi + 8 * (i / 4) + i % 4;
+      for (int i = 3; i >= 0; --i) {
+        const int v = base + 16 * mi + i;
         if (v < V && acc[mi][ni][i] == tm) f = v;
       }
     st.first = f;
@@ -104,10 +112,10 @@ __device__ __forceinline__ void lm_fold(LmState& st, const f32x16 (&acc)[4][2], 
   // stays exact and s' = (S - e_M) / e_M keeps its relative accuracy
   double sum[2] = {0.0, 0.0};
 #pragma unroll
-  for (int mi = 0; mi < 4; ++mi)
+  for (int mi = 0; mi < 8; ++mi)
 #pragma unroll
-    for (int i = 0; i < 16; ++i) {
-      const int v = base + 32 * mi + 8 * (i / 4) + i % 4;
+    for (int i = 0; i < 4; ++i) {
+      const int v = base + 16 * mi + i;
       sum[i & 1] += v < V ? (double)term(acc[mi][ni][i], st.K) : 0.0;
     }
   st.S += sum[0] + sum[1];
@@ -122,21 +130,99 @@ __device__ __forceinline__ void lm_combine(LmState& st, float M2, float K2, doub
   st.first = min(fa, fb);
 }
 
+// ---- LDS-DMA main loop -----------------------------------------------------
+// Stages of kLmBK hidden elements: 256 weight rows and 256 hidden rows of
+// kLmBK * 2 bytes each, written by buffer_load ... lds (each lane of a wave
+// instruction fills the next 16 bytes of LDS).  kLmNBuf stages are resident,
+// so the loads of a stage are issued kLmNBuf - 1 stages before it is used.
+// Rows are stored unpadded; the 16-byte vector s of row r sits in slot
+// s ^ lm_swz(r), which keeps the MFMA operand reads free of bank conflicts.
+constexpr int kLmSlots = kLmBK / 8;                       // 16-byte vectors per row and stage
+constexpr int kLmRowBytes = kLmBK * 2;
+constexpr int kLmWBytes = kLmVt * kLmRowBytes;            // weight part of a stage
+constexpr int kLmStageBytes = (kLmVt + kLmPt) * kLmRowBytes;
+constexpr int kLmDmaRows = kWave / kLmSlots;              // rows per wave-wide load
+constexpr int kLmWDma = kLmVt / kLmDmaRows / kLmWaves;    // weight loads per wave and stage
+constexpr int kLmHDma = kLmPt / kLmDmaRows / kLmWaves;
+constexpr int kLmDmaPerStage = kLmWDma + kLmHDma;
+constexpr size_t kLmLdsBytes = (size_t)kLmNBuf * kLmStageBytes;
+static_assert(kLmWDma == 2 && kLmHDma == 2, "the interleaved schedule issues two loads of each");
+
+__device__ __forceinline__ int lm_swz(int r) { return ((r >> 1) ^ ((r >> 3) & 1)) & (kLmSlots - 1); }
+
+typedef __attribute__((address_space(3))) void* lds_ptr_t;
+typedef int i32x4 __attribute__((ext_vector_type(4)));
+
+// buffer resource of a raw byte range (stride 0, bounds check on the byte
+// offset), all four words wave-uniform
+__device__ __forceinline__ i32x4 lm_rsrc(const void* base, uint32_t bytes) {
+  const uint64_t a = (uint64_t)base;
+  i32x4 r;
+  r[0] = __builtin_amdgcn_readfirstlane((int)(uint32_t)a);
+  r[1] = __builtin_amdgcn_readfirstlane((int)((uint32_t)(a >> 32) & 0xffffu));
+  r[2] = __builtin_amdgcn_readfirstlane((int)bytes);
+  r[3] = 0x00020000;
+  return r;
+}
+
+// one wave-wide 16-byte-per-lane load into LDS: lane i's vector lands at
+// byte lds + 16 i.  Issued as inline assembly: the compiler cannot tell which
+// buffer such a load writes and would drain every load in flight before the
+// next LDS read; the explicit vmcnt waits of lm_sync are the ones needed.
+__device__ __forceinline__ void lm_dma(i32x4 rsrc, uint32_t lds, uint32_t voff, int soff) {
+  asm volatile("s_mov_b32 m0, %0\n\tbuffer_load_dwordx4 %1, %2, %3 offen lds"
+               :: "s"(lds), "v"(voff), "s"(rsrc), "s"(soff) : "memory", "m0");
+}
+
+// waits until at most N of this wave's loads are outstanding, then meets the
+// other waves; the memory clobber keeps LDS accesses on their side
+template <int N>
+__device__ __forceinline__ void lm_sync() {
+  asm volatile("s_waitcnt vmcnt(%0)\n\ts_barrier" ::"n"(N) : "memory");
+}
+
+#define LM_FENCE() __builtin_amdgcn_sched_barrier(0)
+
+// the producer: the next stage this wave loads (tile relative to the
+// workgroup's first, stage within the tile), the buffer it goes to, and the
+// lane's load offsets.  Past the last stage the last one is loaded again
+// (into a buffer nobody reads any more), so every stage issues the same
+// number of loads and the fixed vmcnt waits stay exact.
+struct LmProducer {
+  int tile, ks, left, buf;
+  i32x4 wr, hr;
+  uint32_t w_voff[kLmWDma], h_voff[kLmHDma];
+  uint32_t lds_w[kLmWDma], lds_h[kLmHDma];   // wave's LDS offsets within a stage
+};
+
+__device__ __forceinline__ void lm_tile_setup(LmProducer& p, const uint16_t* weight, int t, int V,
+                                              int d, int lane, int wave) {
+  const int n0 = t * kLmVt;
+  const uint32_t row_bytes = (uint32_t)d * 2u;
+  p.wr = lm_rsrc(weight + (size_t)n0 * d, kLmVt * row_bytes);
+  const int lr = lane / kLmSlots, ls = lane % kLmSlots;
+#pragma unroll
+  for (int j = 0; j < kLmWDma; ++j) {
+    const int r = (wave * kLmWDma + j) * kLmDmaRows + lr;
+    const int v = min(n0 + r, V - 1) - n0;              // rows past the vocabulary repeat the last
+    p.w_voff[j] = (uint32_t)v * row_bytes + (uint32_t)((ls ^ lm_swz(r)) * 16);
+  }
+}
+
 // grid (position tiles, vocabulary splits).  A workgroup takes kLmPt
 // candidate positions and the split's vocabulary tiles of kLmVt rows; wave w
 // computes vocabulary rows 128 (w % 2) .. +127 of a tile against positions
-// 64 (w / 2) .. +63 (4 x 2 MFMA 32x32x16 accumulators, vocabulary along the
-// MFMA rows so each lane's accumulators belong to two positions only).
-// Hidden-dimension stages of kLmBK are double-buffered in LDS.
+// 64 (w / 2) .. +63 as 8 x 4 MFMA 16x16x32 blocks, vocabulary along the MFMA
+// rows: lane l holds positions 16 ni + l % 16 and, for each, vocabulary rows
+// 16 mi + 4 (l / 16) + i of the wave's 128.
 __global__ void __launch_bounds__(kLmThreads)
 k_lm_partial(const uint16_t* __restrict__ hidden, const uint16_t* __restrict__ weight,
              const int32_t* __restrict__ rows, const int32_t* __restrict__ count, int d, int V,
-             int tiles_per_split, WavePartial* __restrict__ partials, int n_split) {
-  extern __shared__ u32x4 lm_lds[];
-  constexpr int kWBuf = kLmVt * kLmRowVec, kHBuf = kLmPt * kLmRowVec;   // u32x4 per buffer
+             int tiles_per_split, uint32_t hid_bytes, WavePartial* __restrict__ partials, int n_split) {
+  extern __shared__ __attribute__((aligned(1024))) char lm_lds[];
   const int tid = threadIdx.x;
   const int lane = tid % kWave;
-  const int wave = tid / kWave;
+  const int wave = __builtin_amdgcn_readfirstlane(tid / kWave);
   const int vw = wave % 2, pw = wave / 2;
   const int nrows = *count;
   const int p0 = blockIdx.x * kLmPt;
@@ -144,128 +230,157 @@ k_lm_partial(const uint16_t* __restrict__ hidden, const uint16_t* __restrict__ w
   const int n_tiles = (V + kLmVt - 1) / kLmVt;
   const int t_begin = blockIdx.y * tiles_per_split;
   const int t_end = min(t_begin + tiles_per_split, n_tiles);
-  const int dv = d / 8;                                   // 16-byte vectors per row of hidden / weight
-
-  // chunk j of this thread: LDS row tid/8 + 64 j, vector tid % 8 (kLmBK / 8 == 8)
-  const int c_row = tid / (kLmBK / 8), c_kc = tid % (kLmBK / 8);
-  const int c_dst = c_row * kLmRowVec + c_kc;
-  constexpr int kRowStep = kLmThreads / (kLmBK / 8);      // LDS rows between a thread's chunks
-  const u32x4* hv = reinterpret_cast<const u32x4*>(hidden);
-  const u32x4* wv = reinterpret_cast<const u32x4*>(weight);
-  int h_off[kLmHChunks];                                  // u32x4 offsets (positions past the end repeat p0)
-#pragma unroll
-  for (int j = 0; j < kLmHChunks; ++j) {
-    const int r = p0 + c_row + j * kRowStep;
-    h_off[j] = rows[r < nrows ? r : p0] * dv + c_kc;
-  }
-
-  LmState st[2];
-#pragma unroll
-  for (int ni = 0; ni < 2; ++ni) st[ni] = LmState{kNegInf, kRefFloor, 0.0, 0x7fffffff};
-
   const int nks = d / kLmBK;
+  const uint32_t lds0 = (uint32_t)(uintptr_t)(lds_ptr_t)lm_lds;
+
+  LmProducer pr;
+  pr.tile = 0;
+  pr.ks = 0;
+  pr.left = (t_end - t_begin) * nks;
+  pr.buf = 0;
+  pr.hr = lm_rsrc(hidden, hid_bytes);
+  {
+    const int lr = lane / kLmSlots, ls = lane % kLmSlots;
+#pragma unroll
+    for (int j = 0; j < kLmHDma; ++j) {
+      const int r = (wave * kLmHDma + j) * kLmDmaRows + lr;
+      const int q = p0 + r < nrows ? p0 + r : p0;       // past the end: repeat the first row
+      pr.h_voff[j] = (uint32_t)rows[q] * (uint32_t)d * 2u + (uint32_t)((ls ^ lm_swz(r)) * 16);
+      pr.lds_h[j] = (uint32_t)(kLmWBytes + (wave * kLmHDma + j) * kLmDmaRows * kLmRowBytes);
+    }
+#pragma unroll
+    for (int j = 0; j < kLmWDma; ++j)
+      pr.lds_w[j] = (uint32_t)((wave * kLmWDma + j) * kLmDmaRows * kLmRowBytes);
+  }
+  lm_tile_setup(pr, weight, t_begin, V, d, lane, wave);
+
+  // the loads of the producer's stage: W j (j < 2) or H j - 2
+  auto dma = [&](int j) {
+    const uint32_t sb = lds0 + (uint32_t)pr.buf * kLmStageBytes;
+    const int soff = pr.ks * kLmRowBytes;
+    if (j < kLmWDma)
+      lm_dma(pr.wr, sb + pr.lds_w[j], pr.w_voff[j], soff);
+    else
+      lm_dma(pr.hr, sb + pr.lds_h[j - kLmWDma], pr.h_voff[j - kLmWDma], soff);
+  };
+  auto advance = [&]() {
+    if (pr.left > 1) {
+      --pr.left;
+      if (++pr.ks == nks) {
+        pr.ks = 0;
+        ++pr.tile;
+        lm_tile_setup(pr, weight, t_begin + pr.tile, V, d, lane, wave);
+      }
+    }
+    pr.buf = pr.buf + 1 == kLmNBuf ? 0 : pr.buf + 1;
+  };
+
+  // operand addresses of this lane: row l % 16 of a 16-row block, 16-byte
+  // vector l / 16 of the stage's 32 hidden elements
+  const uint32_t slot = (uint32_t)(((lane / 16) ^ lm_swz(lane % 16)) * 16);
+  const uint32_t a_addr = (uint32_t)((128 * vw + lane % 16) * kLmRowBytes) + slot;
+  const uint32_t b_addr = (uint32_t)(kLmWBytes + (64 * pw + lane % 16) * kLmRowBytes) + slot;
+  auto lds_at = [&](uint32_t a) -> bf16x8 {
+    return *reinterpret_cast<const bf16x8*>(lm_lds + (a - lds0));
+  };
+
+  LmState st[4];
+#pragma unroll
+  for (int ni = 0; ni < 4; ++ni) st[ni] = LmState{kNegInf, kRefFloor, 0.0, 0x7fffffff};
+
+  f32x4 acc[8][4];
+  bf16x8 fa[8], fb[4], nb4[4], na7;
+#define LM_M(mi, ni) acc[mi][ni] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fa[mi], fb[ni], acc[mi][ni], 0, 0, 0)
+
+  // prologue: kLmNBuf - 1 stages in flight, then wait for the first
+  for (int s = 0; s < kLmNBuf - 1; ++s) {
+#pragma unroll
+    for (int j = 0; j < kLmDmaPerStage; ++j) dma(j);
+    advance();
+  }
+  lm_sync<(kLmNBuf - 2) * kLmDmaPerStage>();
+#pragma unroll
+  for (int ni = 0; ni < 4; ++ni) fb[ni] = lds_at(lds0 + b_addr + ni * 16 * kLmRowBytes);
+#pragma unroll
+  for (int mi = 0; mi < 8; ++mi) fa[mi] = lds_at(lds0 + a_addr + mi * 16 * kLmRowBytes);
+
+  int cbuf = 0;
   for (int t = t_begin; t < t_end; ++t) {
-    const int n0 = t * kLmVt;
-    int w_off[kLmWChunks];
 #pragma unroll
-    for (int j = 0; j < kLmWChunks; ++j) {
-      const int v = n0 + c_row + j * kRowStep;
-      w_off[j] = (v < V ? v : V - 1) * dv + c_kc;
-    }
-    f32x16 acc[4][2];
+    for (int mi = 0; mi < 8; ++mi)
 #pragma unroll
-    for (int mi = 0; mi < 4; ++mi)
+      for (int ni = 0; ni < 4; ++ni)
 #pragma unroll
-      for (int ni = 0; ni < 2; ++ni)
-#pragma unroll
-        for (int i = 0; i < 16; ++i) acc[mi][ni][i] = 0.0f;
-    u32x4 rw[kLmWChunks], rh[kLmHChunks];
-    // stage 0 into buffer 0, stage 1 into registers
-#pragma unroll
-    for (int j = 0; j < kLmWChunks; ++j) rw[j] = wv[w_off[j]];
-#pragma unroll
-    for (int j = 0; j < kLmHChunks; ++j) rh[j] = hv[h_off[j]];
-    __syncthreads();                                      // the previous tile's reads are done
-#pragma unroll
-    for (int j = 0; j < kLmWChunks; ++j) lm_lds[c_dst + j * kRowStep * kLmRowVec] = rw[j];
-#pragma unroll
-    for (int j = 0; j < kLmHChunks; ++j) lm_lds[2 * kWBuf + c_dst + j * kRowStep * kLmRowVec] = rh[j];
-    if (nks > 1) {
-#pragma unroll
-      for (int j = 0; j < kLmWChunks; ++j) rw[j] = wv[w_off[j] + kLmBK / 8];
-#pragma unroll
-      for (int j = 0; j < kLmHChunks; ++j) rh[j] = hv[h_off[j] + kLmBK / 8];
-    }
-    __syncthreads();
+        for (int i = 0; i < 4; ++i) acc[mi][ni][i] = 0.0f;
     for (int ks = 0; ks < nks; ++ks) {
-      const u32x4* cw = lm_lds + (ks & 1) * kWBuf;
-      const u32x4* ch = lm_lds + 2 * kWBuf + (ks & 1) * kHBuf;
+      const int nbuf = cbuf + 1 == kLmNBuf ? 0 : cbuf + 1;
+      const uint32_t nb = lds0 + (uint32_t)nbuf * kLmStageBytes;
+      // the next stage has landed once only the stages after it are
+      // outstanding; every wave has finished reading the previous stage's
+      // buffer, which the loads issued below refill
+      LM_FENCE();
+      lm_sync<(kLmNBuf - 3) * kLmDmaPerStage>();
+      // the stage's 32 MFMAs; the next stage's operands are read as the
+      // registers they replace fall dead, the loads kLmNBuf - 1 stages ahead
+      // go out in between
+      LM_M(0, 0); LM_FENCE(); nb4[0] = lds_at(nb + b_addr); LM_FENCE();
+      LM_M(0, 1); LM_FENCE(); nb4[1] = lds_at(nb + b_addr + 16 * kLmRowBytes); LM_FENCE();
+      LM_M(0, 2); LM_FENCE(); nb4[2] = lds_at(nb + b_addr + 32 * kLmRowBytes); LM_FENCE();
+      LM_M(0, 3); LM_FENCE(); nb4[3] = lds_at(nb + b_addr + 48 * kLmRowBytes); LM_FENCE();
 #pragma unroll
-      for (int kk = 0; kk < kLmBK / 16; ++kk) {
-        const int kv = kk * 2 + lane / 32;                // 16-byte vector index along k
-        bf16x8 b[2];
-#pragma unroll
-        for (int ni = 0; ni < 2; ++ni)
-          b[ni] = __builtin_bit_cast(bf16x8, ch[(64 * pw + 32 * ni + lane % 32) * kLmRowVec + kv]);
-#pragma unroll
-        for (int mi = 0; mi < 4; ++mi) {
-          const bf16x8 a = __builtin_bit_cast(bf16x8, cw[(128 * vw + 32 * mi + lane % 32) * kLmRowVec + kv]);
-#pragma unroll
-          for (int ni = 0; ni < 2; ++ni)
-            acc[mi][ni] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b[ni], acc[mi][ni], 0, 0, 0);
-        }
+      for (int mi = 1; mi < 8; ++mi) {
+        LM_M(mi, 0); LM_FENCE();
+        fa[mi - 1] = lds_at(nb + a_addr + (mi - 1) * 16 * kLmRowBytes); LM_FENCE();
+        LM_M(mi, 1); LM_FENCE();
+        if (mi >= 2 && mi < 2 + kLmDmaPerStage) { dma(mi - 2); LM_FENCE(); }
+        if (mi == 7) { na7 = lds_at(nb + a_addr + 7 * 16 * kLmRowBytes); LM_FENCE(); }
+        LM_M(mi, 2); LM_FENCE();
+        LM_M(mi, 3); LM_FENCE();
       }
-      if (ks + 1 < nks) {                                 // stage ks+1: registers -> other buffer
-        u32x4* nw = lm_lds + ((ks + 1) & 1) * kWBuf;
-        u32x4* nh = lm_lds + 2 * kWBuf + ((ks + 1) & 1) * kHBuf;
 #pragma unroll
-        for (int j = 0; j < kLmWChunks; ++j) nw[c_dst + j * kRowStep * kLmRowVec] = rw[j];
-#pragma unroll
-        for (int j = 0; j < kLmHChunks; ++j) nh[c_dst + j * kRowStep * kLmRowVec] = rh[j];
-      }
-      if (ks + 2 < nks) {                                 // stage ks+2 in flight during the MFMAs
-        const int off = (ks + 2) * (kLmBK / 8);
-#pragma unroll
-        for (int j = 0; j < kLmWChunks; ++j) rw[j] = wv[w_off[j] + off];
-#pragma unroll
-        for (int j = 0; j < kLmHChunks; ++j) rh[j] = hv[h_off[j] + off];
-      }
-      __syncthreads();
+      for (int ni = 0; ni < 4; ++ni) fb[ni] = nb4[ni];
+      fa[7] = na7;
+      advance();
+      cbuf = nbuf;
     }
-    const int base = n0 + 128 * vw + 4 * (lane / 32);
+    const int base = t * kLmVt + 128 * vw + 4 * (lane / 16);
 #pragma unroll
-    for (int ni = 0; ni < 2; ++ni) lm_fold(st[ni], acc, ni, base, V);
+    for (int ni = 0; ni < 4; ++ni) lm_fold(st[ni], acc, ni, base, V);
   }
-  // lanes l and l + 32 hold the same positions (interleaved vocabulary rows)
+#undef LM_M
+  // lanes l, l^16, l^32, l^48 hold the same positions
 #pragma unroll
-  for (int ni = 0; ni < 2; ++ni) {
-    const float M2 = __shfl_xor(st[ni].M, 32);
-    const float K2 = __shfl_xor(st[ni].K, 32);
-    const double S2 = __shfl_xor(st[ni].S, 32);
-    const int f2 = __shfl_xor(st[ni].first, 32);
-    lm_combine(st[ni], M2, K2, S2, f2);
+  for (int ni = 0; ni < 4; ++ni) {
+#pragma unroll
+    for (int x = 16; x <= 32; x *= 2) {
+      const float M2 = __shfl_xor(st[ni].M, x);
+      const float K2 = __shfl_xor(st[ni].K, x);
+      const double S2 = __shfl_xor(st[ni].S, x);
+      const int f2 = __shfl_xor(st[ni].first, x);
+      lm_combine(st[ni], M2, K2, S2, f2);
+    }
   }
-  // the two vocabulary halves of a position meet in LDS (buffers are free now)
+  // the two vocabulary halves of a position meet in LDS, once no load is
+  // still writing into it
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
   WavePartial* xch = reinterpret_cast<WavePartial*>(lm_lds);
   __syncthreads();
-  if (vw == 1 && lane < 32) {
+  if (vw == 1 && lane < 16) {
 #pragma unroll
-    for (int ni = 0; ni < 2; ++ni)
-      xch[64 * pw + 32 * ni + lane] = WavePartial{st[ni].M, st[ni].K, st[ni].S, st[ni].first};
+    for (int ni = 0; ni < 4; ++ni)
+      xch[64 * pw + 16 * ni + lane] = WavePartial{st[ni].M, st[ni].K, st[ni].S, st[ni].first};
   }
   __syncthreads();
-  if (vw != 0 || lane >= 32) return;
+  if (vw != 0 || lane >= 16) return;
 #pragma unroll
-  for (int ni = 0; ni < 2; ++ni) {
-    const WavePartial o = xch[64 * pw + 32 * ni + lane];
+  for (int ni = 0; ni < 4; ++ni) {
+    const WavePartial o = xch[64 * pw + 16 * ni + lane];
     lm_combine(st[ni], o.m, o.K, o.S, o.first);
-    const int r = p0 + 64 * pw + 32 * ni + lane;
+    const int r = p0 + 64 * pw + 16 * ni + lane;
     if (r < nrows)
       partials[(size_t)r * n_split + blockIdx.y] = WavePartial{st[ni].M, st[ni].K, st[ni].S, st[ni].first};
   }
 }
-
-constexpr size_t kLmLdsBytes = (size_t)(2 * kLmVt + 2 * kLmPt) * kLmRowVec * sizeof(u32x4);
 
 // Per candidate row, one wavefront: lane l combines the splits l, l+64, ...
 // of the row's contiguous partials, then a fixed butterfly over the lanes
@@ -334,9 +449,28 @@ static LmPlan lm_plan(int B, int L, int V, bool need_out) {
 }
 
 static bool lm_sizes_ok(int B, int L, int d, int V) {
-  if (B < 0 || L < 1 || V < 1 || d < kLmBK || d % kLmBK != 0) return false;
-  // 16-byte vector offsets into hidden and weight fit in 31 bits
-  return (long long)B * L * (d / 8) < 0x7fffffffLL && (long long)V * (d / 8) < 0x7fffffffLL;
+  if (B < 0 || L < 1 || V < 1 || d < 64 || d % 64 != 0) return false;
+  // hidden is addressed by 32-bit byte offsets (buffer loads)
+  return (long long)B * L * d * 2 <= 0xffffffffLL && (long long)V * (d / 8) < 0x7fffffffLL;
+}
+
+// The partial kernel's dynamic LDS (128 KiB) is above the default limit; the
+// limit is raised once per device, before the first launch there.
+constexpr int kLmMaxDevices = 64;
+static std::atomic<bool> lm_lds_allowed[kLmMaxDevices];
+
+static hipError_t lm_allow_lds() {
+  int dev = 0;
+  const hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev >= 0 && dev < kLmMaxDevices && lm_lds_allowed[dev].load(std::memory_order_acquire))
+    return hipSuccess;
+  const hipError_t a = hipFuncSetAttribute((const void*)k_lm_partial,
+                                           hipFuncAttributeMaxDynamicSharedMemorySize,
+                                           (int)kLmLdsBytes);
+  if (a == hipSuccess && dev >= 0 && dev < kLmMaxDevices)
+    lm_lds_allowed[dev].store(true, std::memory_order_release);
+  return a;
 }
 
 static hipError_t lm_launch(const void* hidden, const void* weight, int B, int L, int d, int V,
@@ -345,18 +479,14 @@ static hipError_t lm_launch(const void* hidden, const void* weight, int B, int L
   int32_t* count = (int32_t*)ws;
   int32_t* rows = (int32_t*)(ws + p.off_rows);
   WavePartial* part = (WavePartial*)(ws + p.off_partials);
-  // the partial kernel's LDS (147 KB) exceeds the default limit; set it on the
-  // current device before anything is enqueued
-  const hipError_t attr = hipFuncSetAttribute((const void*)k_lm_partial,
-                                              hipFuncAttributeMaxDynamicSharedMemorySize,
-                                              (int)kLmLdsBytes);
+  const hipError_t attr = lm_allow_lds();
   if (attr != hipSuccess) return attr;
   hipLaunchKernelGGL(k_lm_zero, dim3(1), dim3(64), 0, st, count);
   hipLaunchKernelGGL(k_lm_compact, dim3((unsigned)((B + 3) / 4)), dim3(256), 0, st, mask, bs, be, B,
                      L, rows, count, out);
   hipLaunchKernelGGL(k_lm_partial, dim3((unsigned)p.m_tiles, (unsigned)p.n_split), dim3(kLmThreads),
                      kLmLdsBytes, st, (const uint16_t*)hidden, (const uint16_t*)weight, rows, count,
-                     d, V, p.tiles_per_split, part, p.n_split);
+                     d, V, p.tiles_per_split, (uint32_t)((size_t)B * L * d * 2), part, p.n_split);
   const long long n = (long long)B * L;
   hipLaunchKernelGGL(k_lm_finish, dim3((unsigned)((n + 3) / 4)), dim3(256), 0, st, rows, count,
                      part, p.n_split, out);

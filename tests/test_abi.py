@@ -197,6 +197,9 @@ def test_lmhead_entry_points_check_arguments(lib):
     assert lib.fdllm_lmhead_workspace_size(4, 32, 0, 1000, ctypes.byref(n)) == fd.ERR_SIZE
     assert lib.fdllm_lmhead_workspace_size(4, 32, 64, 0, ctypes.byref(n)) == fd.ERR_SIZE
     assert lib.fdllm_lmhead_workspace_size(4, 32, 64, 10, None) == fd.ERR_INVALID_ARG
+    # hidden states beyond 32-bit byte offsets (2^16 * 64 * 512 * 2 bytes = 4 GiB)
+    assert lib.fdllm_lmhead_workspace_size(1 << 16, 64, 512, 1000, ctypes.byref(n)) == fd.ERR_SIZE
+    assert lib.fdllm_lmhead_workspace_size((1 << 16) - 1, 64, 512, 1000, ctypes.byref(n)) == 0
     args = lambda **kw: [kw.get("h", p), kw.get("w", p), 2, 8, kw.get("d", 64), 100, kw.get("m", p), p, p,
                          kw.get("tok", p), kw.get("conf", p), null, null, kw.get("ws", p),
                          kw.get("wsb", 1 << 30), null]

@@ -129,6 +129,31 @@ def test_lmhead_decode_step_vs_oracle(gpu, B, L, d, V, kind, window):
         say(f"  {rule}({p}): commits {int(n.clamp(min=0).sum())}, flagged {nf} (matching {nfm})")
 
 
+def test_lmhead_decode_step_eta_tensor(gpu):
+    """The robust rule with a per-position allowance, LM-head form."""
+    B, L, d, V, window = 6, 24, 128, 3000, 24
+    hidden, weight, mask, start, end, x, name = _case(B, L, d, V, "exact", window, seed=5)
+    say(f"[lmhead decode eta tensor] {name}")
+    m0, x0 = mask.cpu().numpy(), x.cpu().numpy()
+    s, e = start.cpu().numpy(), end.cpu().numpy()
+    cells = candidates(m0, s, e, range(B))
+    lg = _oracle_rows(hidden, weight, cells)[0] if cells else {}
+    eta = np.random.default_rng(2).uniform(-0.02, 0.08, (B, L)).astype(np.float32)
+    mk, xx = mask.clone(), x.clone()
+    commit = torch.empty((B, L), dtype=torch.uint8, device="cuda")
+    n = torch.empty((B,), dtype=torch.int32, device="cuda")
+    gpu.fdllm_lmhead_decode_step(hidden, weight, mk, start, end, xx, "robust", 0.9, commit=commit,
+                                 n_commit=n, eta=torch.from_numpy(eta).cuda())
+    torch.cuda.synchronize()
+    r = oracle.decode_step(lambda b, i: lg[(b, i)], B, L, m0, s, e, x0, "robust", 0.9, eta=eta)
+    nf, nfm = compare_selection(commit.cpu().numpy(), n.cpu().numpy(), r.commit, r.n_commit,
+                                r.flagged, range(B))
+    ok = ~r.flagged
+    assert np.array_equal(xx.cpu().numpy()[ok], r.x[ok])
+    assert np.array_equal(mk.cpu().numpy()[ok], r.mask[ok])
+    say(f"  commits {int(n.clamp(min=0).sum())}, flagged {nf} (matching {nfm})")
+
+
 def test_lmhead_rejects_bad_shapes(gpu):
     hidden = torch.zeros((1, 4, 96), dtype=torch.bfloat16, device="cuda")     # d not a multiple of 64
     weight = torch.zeros((10, 96), dtype=torch.bfloat16, device="cuda")

@@ -103,6 +103,24 @@ def test_generation_vs_oracle(gpu, rule, p):
     gen.close()
 
 
+def test_generation_eta_tensor_vs_oracle(gpu):
+    """The robust rule with a per-position allowance [B, G] (some entries
+    negative, which count as 0) through the whole device loop."""
+    B, G, blk, V, seed = 5, 40, 8, 1500, 7
+    rng = np.random.default_rng(11)
+    eta = rng.uniform(-0.01, 0.06, (B, G)).astype(np.float32)
+    eta[1] = 0.0
+    say(f"[generation eta tensor] B={B} G={G} blk={blk} V={V}")
+    gen = gpu.Generation(B, G, blk, V, seed, "robust", 0.8, eta=torch.from_numpy(eta).cuda(),
+                         chunk=3, use_graph=True)
+    steps = gen.run()
+    torch.cuda.synchronize()
+    t, diverged, nflag = _replay(seed, B, G, blk, V, "robust", 0.8, eta, gen.hist.cpu().numpy(),
+                                 steps, gen.x.cpu().numpy())
+    say(f"  steps {steps} (oracle {t}), diverged {sorted(diverged)}, flagged {nflag}")
+    gen.close()
+
+
 @pytest.mark.parametrize("B,G,blk,V", [(8, 256, 32, 126464), (130, 64, 16, 512)])
 def test_generation_graph_equals_eager(gpu, B, G, blk, V):
     """Graph replay in chunks, direct launches with a host check every step,
