@@ -10,11 +10,12 @@
 //
 // Main loop of the partial kernel: a workgroup of 8 waves owns 256 candidate
 // positions x 256 vocabulary rows per tile; the hidden dimension streams in
-// stages of 32 elements (32 KiB of weight and hidden rows per stage) that
-// buffer_load ... lds writes straight into LDS, four stages resident so the
-// loads of a stage go out three stages before it is used.  One barrier per
-// stage; each wave's 32 MFMAs of a stage are interleaved with the reads of
-// the next stage's operands and with the stage loads.
+// stages of 64 elements (128 bytes of every weight and hidden row, so each
+// load uses whole cache lines; 64 KiB per stage) that buffer_load ... lds
+// writes straight into LDS, two stages resident.  One barrier per stage;
+// each wave's 64 MFMAs of a stage are interleaved with the reads of the next
+// half stage's operands, and the second half with the loads of the stage
+// after next.
 #include <hip/hip_runtime.h>
 
 #include <stdint.h>
@@ -37,8 +38,8 @@ typedef float f32x4 __attribute__((ext_vector_type(4)));
 constexpr int kLmWaves = 8;                    // waves per workgroup
 constexpr int kLmVt = 256;                     // vocabulary rows per tile (MFMA A operand)
 constexpr int kLmPt = 256;                     // positions per workgroup (MFMA B operand)
-constexpr int kLmBK = 32;                      // hidden-dimension elements per LDS stage
-constexpr int kLmNBuf = 4;                     // stages resident in LDS
+constexpr int kLmBK = 64;                      // hidden-dimension elements per LDS stage
+constexpr int kLmNBuf = 2;                     // stages resident in LDS
 constexpr int kLmThreads = kLmWaves * kWave;
 constexpr int kLmRows = kLmPt;                 // candidate rows per workgroup
 constexpr int kLmCols = kLmVt;                 // vocabulary columns per tile
@@ -133,10 +134,12 @@ __device__ __forceinline__ void lm_combine(LmState& st, float M2, float K2, doub
 // ---- LDS-DMA main loop -----------------------------------------------------
 // Stages of kLmBK hidden elements: 256 weight rows and 256 hidden rows of
 // kLmBK * 2 bytes each, written by buffer_load ... lds (each lane of a wave
-// instruction fills the next 16 bytes of LDS).  kLmNBuf stages are resident,
-// so the loads of a stage are issued kLmNBuf - 1 stages before it is used.
-// Rows are stored unpadded; the 16-byte vector s of row r sits in slot
-// s ^ lm_swz(r), which keeps the MFMA operand reads free of bank conflicts.
+// instruction fills the next 16 bytes of LDS).  The stage after next is
+// loaded into the buffer of the stage just read, in the second half of the
+// current stage.  Rows are stored unpadded; the 16-byte vector s of row r
+// sits in slot s ^ lm_swz(r).  lm_swz was chosen from LDS bank-conflict
+// counter measurements of ds_read_b128 patterns on gfx950: with it the
+// operand reads (lane l: row l % 16, vector 4 h + l / 16) are conflict-free.
 constexpr int kLmSlots = kLmBK / 8;                       // 16-byte vectors per row and stage
 constexpr int kLmRowBytes = kLmBK * 2;
 constexpr int kLmWBytes = kLmVt * kLmRowBytes;            // weight part of a stage
@@ -146,9 +149,9 @@ constexpr int kLmWDma = kLmVt / kLmDmaRows / kLmWaves;    // weight loads per wa
 constexpr int kLmHDma = kLmPt / kLmDmaRows / kLmWaves;
 constexpr int kLmDmaPerStage = kLmWDma + kLmHDma;
 constexpr size_t kLmLdsBytes = (size_t)kLmNBuf * kLmStageBytes;
-static_assert(kLmWDma == 2 && kLmHDma == 2, "the interleaved schedule issues two loads of each");
+static_assert(kLmWDma == 4 && kLmHDma == 4, "the interleaved schedule issues four loads of each");
 
-__device__ __forceinline__ int lm_swz(int r) { return ((r >> 1) ^ ((r >> 3) & 1)) & (kLmSlots - 1); }
+__device__ __forceinline__ int lm_swz(int r) { return (r & 1) | ((r >> 1) & 2) | ((r << 1) & 4); }
 
 typedef __attribute__((address_space(3))) void* lds_ptr_t;
 typedef int i32x4 __attribute__((ext_vector_type(4)));
@@ -170,15 +173,18 @@ __device__ __forceinline__ i32x4 lm_rsrc(const void* base, uint32_t bytes) {
 // buffer such a load writes and would drain every load in flight before the
 // next LDS read; the explicit vmcnt waits of lm_sync are the ones needed.
 __device__ __forceinline__ void lm_dma(i32x4 rsrc, uint32_t lds, uint32_t voff, int soff) {
-  asm volatile("s_mov_b32 m0, %0\n\tbuffer_load_dwordx4 %1, %2, %3 offen lds"
-               :: "s"(lds), "v"(voff), "s"(rsrc), "s"(soff) : "memory", "m0");
+  int keep;   // m0 is the compiler's register: saved and restored around the load
+  asm volatile("s_mov_b32 %0, m0\n\ts_mov_b32 m0, %1\n\tbuffer_load_dwordx4 %2, %3, %4 offen lds\n\t"
+               "s_mov_b32 m0, %0"
+               : "=&s"(keep) : "s"(lds), "v"(voff), "s"(rsrc), "s"(soff) : "memory");
 }
 
-// waits until at most N of this wave's loads are outstanding, then meets the
-// other waves; the memory clobber keeps LDS accesses on their side
+// waits until at most N of this wave's loads are outstanding and its LDS
+// reads are done, then meets the other waves; the memory clobber keeps LDS
+// accesses on their side
 template <int N>
 __device__ __forceinline__ void lm_sync() {
-  asm volatile("s_waitcnt vmcnt(%0)\n\ts_barrier" ::"n"(N) : "memory");
+  asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)\n\ts_barrier" ::"n"(N) : "memory");
 }
 
 #define LM_FENCE() __builtin_amdgcn_sched_barrier(0)
@@ -187,7 +193,7 @@ __device__ __forceinline__ void lm_sync() {
 // workgroup's first, stage within the tile), the buffer it goes to, and the
 // lane's load offsets.  Past the last stage the last one is loaded again
 // (into a buffer nobody reads any more), so every stage issues the same
-// number of loads and the fixed vmcnt waits stay exact.
+// number of loads.
 struct LmProducer {
   int tile, ks, left, buf;
   i32x4 wr, hr;
@@ -254,7 +260,7 @@ k_lm_partial(const uint16_t* __restrict__ hidden, const uint16_t* __restrict__ w
   }
   lm_tile_setup(pr, weight, t_begin, V, d, lane, wave);
 
-  // the loads of the producer's stage: W j (j < 2) or H j - 2
+  // the loads of the producer's stage: W j (j < 4) or H j - 4
   auto dma = [&](int j) {
     const uint32_t sb = lds0 + (uint32_t)pr.buf * kLmStageBytes;
     const int soff = pr.ks * kLmRowBytes;
@@ -276,10 +282,14 @@ k_lm_partial(const uint16_t* __restrict__ hidden, const uint16_t* __restrict__ w
   };
 
   // operand addresses of this lane: row l % 16 of a 16-row block, 16-byte
-  // vector l / 16 of the stage's 32 hidden elements
-  const uint32_t slot = (uint32_t)(((lane / 16) ^ lm_swz(lane % 16)) * 16);
-  const uint32_t a_addr = (uint32_t)((128 * vw + lane % 16) * kLmRowBytes) + slot;
-  const uint32_t b_addr = (uint32_t)(kLmWBytes + (64 * pw + lane % 16) * kLmRowBytes) + slot;
+  // vector 4 h + l / 16 of the stage's 64 hidden elements in half h
+  uint32_t a_addr[2], b_addr[2];
+#pragma unroll
+  for (int h = 0; h < 2; ++h) {
+    const uint32_t slot = (uint32_t)(((4 * h + lane / 16) ^ lm_swz(lane % 16)) * 16);
+    a_addr[h] = (uint32_t)((128 * vw + lane % 16) * kLmRowBytes) + slot;
+    b_addr[h] = (uint32_t)(kLmWBytes + (64 * pw + lane % 16) * kLmRowBytes) + slot;
+  }
   auto lds_at = [&](uint32_t a) -> bf16x8 {
     return *reinterpret_cast<const bf16x8*>(lm_lds + (a - lds0));
   };
@@ -291,18 +301,41 @@ k_lm_partial(const uint16_t* __restrict__ hidden, const uint16_t* __restrict__ w
   f32x4 acc[8][4];
   bf16x8 fa[8], fb[4], nb4[4], na7;
 #define LM_M(mi, ni) acc[mi][ni] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fa[mi], fb[ni], acc[mi][ni], 0, 0, 0)
+  // the 32 MFMAs of one half stage on (fa, fb); the operands of the next half
+  // stage (weight operands at sa, hidden operands at sb) are read as the
+  // registers they replace fall dead; with_loads also issues the stage loads
+  auto half = [&](uint32_t sa, uint32_t sb, bool with_loads) {
+    LM_M(0, 0); LM_FENCE(); nb4[0] = lds_at(sb); LM_FENCE();
+    LM_M(0, 1); LM_FENCE(); nb4[1] = lds_at(sb + 16 * kLmRowBytes); LM_FENCE();
+    LM_M(0, 2); LM_FENCE(); nb4[2] = lds_at(sb + 32 * kLmRowBytes); LM_FENCE();
+    LM_M(0, 3); LM_FENCE(); nb4[3] = lds_at(sb + 48 * kLmRowBytes); LM_FENCE();
+#pragma unroll
+    for (int mi = 1; mi < 8; ++mi) {
+      LM_M(mi, 0); LM_FENCE();
+      fa[mi - 1] = lds_at(sa + (mi - 1) * 16 * kLmRowBytes); LM_FENCE();
+      LM_M(mi, 1); LM_FENCE();
+      if (with_loads) { dma(mi - 1); LM_FENCE(); }
+      if (mi == 7) { na7 = lds_at(sa + 7 * 16 * kLmRowBytes); LM_FENCE(); }
+      LM_M(mi, 2); LM_FENCE();
+      if (with_loads && mi == 7) { dma(7); LM_FENCE(); }
+      LM_M(mi, 3); LM_FENCE();
+    }
+#pragma unroll
+    for (int ni = 0; ni < 4; ++ni) fb[ni] = nb4[ni];
+    fa[7] = na7;
+  };
 
-  // prologue: kLmNBuf - 1 stages in flight, then wait for the first
-  for (int s = 0; s < kLmNBuf - 1; ++s) {
+  // prologue: both buffers' stages in flight, then wait for the first
+  for (int s = 0; s < kLmNBuf; ++s) {
 #pragma unroll
     for (int j = 0; j < kLmDmaPerStage; ++j) dma(j);
     advance();
   }
-  lm_sync<(kLmNBuf - 2) * kLmDmaPerStage>();
+  lm_sync<kLmDmaPerStage>();
 #pragma unroll
-  for (int ni = 0; ni < 4; ++ni) fb[ni] = lds_at(lds0 + b_addr + ni * 16 * kLmRowBytes);
+  for (int ni = 0; ni < 4; ++ni) fb[ni] = lds_at(lds0 + b_addr[0] + ni * 16 * kLmRowBytes);
 #pragma unroll
-  for (int mi = 0; mi < 8; ++mi) fa[mi] = lds_at(lds0 + a_addr + mi * 16 * kLmRowBytes);
+  for (int mi = 0; mi < 8; ++mi) fa[mi] = lds_at(lds0 + a_addr[0] + mi * 16 * kLmRowBytes);
 
   int cbuf = 0;
   for (int t = t_begin; t < t_end; ++t) {
@@ -313,33 +346,20 @@ k_lm_partial(const uint16_t* __restrict__ hidden, const uint16_t* __restrict__ w
 #pragma unroll
         for (int i = 0; i < 4; ++i) acc[mi][ni][i] = 0.0f;
     for (int ks = 0; ks < nks; ++ks) {
-      const int nbuf = cbuf + 1 == kLmNBuf ? 0 : cbuf + 1;
+      const uint32_t cb = lds0 + (uint32_t)cbuf * kLmStageBytes;
+      const int nbuf = cbuf ^ 1;
       const uint32_t nb = lds0 + (uint32_t)nbuf * kLmStageBytes;
-      // the next stage has landed once only the stages after it are
-      // outstanding; every wave has finished reading the previous stage's
-      // buffer, which the loads issued below refill
+      // first half: MFMAs on the stage's half 0, its half 1 read in between
       LM_FENCE();
-      lm_sync<(kLmNBuf - 3) * kLmDmaPerStage>();
-      // the stage's 32 MFMAs; the next stage's operands are read as the
-      // registers they replace fall dead, the loads kLmNBuf - 1 stages ahead
-      // go out in between
-      LM_M(0, 0); LM_FENCE(); nb4[0] = lds_at(nb + b_addr); LM_FENCE();
-      LM_M(0, 1); LM_FENCE(); nb4[1] = lds_at(nb + b_addr + 16 * kLmRowBytes); LM_FENCE();
-      LM_M(0, 2); LM_FENCE(); nb4[2] = lds_at(nb + b_addr + 32 * kLmRowBytes); LM_FENCE();
-      LM_M(0, 3); LM_FENCE(); nb4[3] = lds_at(nb + b_addr + 48 * kLmRowBytes); LM_FENCE();
-#pragma unroll
-      for (int mi = 1; mi < 8; ++mi) {
-        LM_M(mi, 0); LM_FENCE();
-        fa[mi - 1] = lds_at(nb + a_addr + (mi - 1) * 16 * kLmRowBytes); LM_FENCE();
-        LM_M(mi, 1); LM_FENCE();
-        if (mi >= 2 && mi < 2 + kLmDmaPerStage) { dma(mi - 2); LM_FENCE(); }
-        if (mi == 7) { na7 = lds_at(nb + a_addr + 7 * 16 * kLmRowBytes); LM_FENCE(); }
-        LM_M(mi, 2); LM_FENCE();
-        LM_M(mi, 3); LM_FENCE();
-      }
-#pragma unroll
-      for (int ni = 0; ni < 4; ++ni) fb[ni] = nb4[ni];
-      fa[7] = na7;
+      half(cb + a_addr[1], cb + b_addr[1], false);
+      // every wave has read all of this stage's buffer, and the next stage
+      // (the only loads outstanding) has landed
+      LM_FENCE();
+      lm_sync<0>();
+      // second half: MFMAs on half 1; the next stage's half 0 read and the
+      // stage after it loaded into this stage's buffer in between
+      half(nb + a_addr[0], nb + b_addr[0], true);
+      LM_FENCE();
       advance();
       cbuf = nbuf;
     }
