@@ -16,7 +16,7 @@ average launch time measured with HIP events on the launch stream, and to a
 read-only stream of the same logits buffer (libfdllm_bench.so).
 `cpu_baseline` times the CPU oracle on a bounded sample of the same workload:
 on all host cores (one process per core, each on its own sequences) and on
-one core.  `--per-config` adds the other workload recipes (one sequence fp32;
+one core.  `--per-workload` adds the other workload recipes (one sequence fp32;
 eight-sequence and 256-sequence simulated generations; 64 sequences in a
 512-position span), cold and cache-hot, the device-resident generation loop
 and the LM head fused with the pass, and can write them as a markdown table.
@@ -39,7 +39,7 @@ HBM_PEAK_GBPS = 8000.0
 IO_BYTES_PER_POSITION = 18   # mask read, commit, tokens, conf, eps, lse (1+1+4+4+4+4)
 # sources of the vocabulary pass kernels (the fused decode step and its helpers)
 SRCS = [os.path.join(ROOT, "paper_2606_02955_amd", "csrc", f) for f in ("fdllm.hip", "pass_common.h")]
-TRAFFIC = os.path.join(ROOT, "profiles", "traffic_fused_decode_config5.json")
+TRAFFIC = os.path.join(ROOT, "profiles", "traffic_fused_decode_b1024_l32.json")
 MAX_HOST_WORKERS = 16        # host CPU share of one GPU
 
 
@@ -95,7 +95,7 @@ def _oracle_worker(blocks, rule, param, ready, go, results):
     torch.set_num_threads(1)
     import oracle
     import workloads
-    rows = torch.stack([workloads.config5_rows(b, "cpu") for b in blocks])     # [n, L, V] bf16
+    rows = torch.stack([workloads.stress_b1024_l32_rows(b, "cpu") for b in blocks])     # [n, L, V] bf16
     n, L, _ = rows.shape
     mask = np.ones((n, L), dtype=np.uint8)
     start = np.zeros(n, dtype=np.int64)
@@ -181,7 +181,7 @@ def cpu_baseline_single(inp, n_blocks: int, rule: str, param: float):
 
 
 # ---------------------------------------------------------------------------
-# per-configuration report
+# per-workload report
 # ---------------------------------------------------------------------------
 def _candidates(inp) -> int:
     import torch
@@ -215,7 +215,7 @@ def _time_steps(fd, torch, inp, selector, p, reps, scratch=None):
 
 
 def _row(name, shape, sel, positions, bytes_, t_cold, t_hot, stream_gbps, extra=None):
-    d = {"config": name, "shape": shape, "selector": sel, "positions_per_step": positions,
+    d = {"workload": name, "shape": shape, "selector": sel, "positions_per_step": positions,
          "logits_bytes_per_step": bytes_, "kernel_ms_cold": 1e3 * t_cold,
          "kernel_ms_hot": None if t_hot is None else 1e3 * t_hot,
          "positions_per_s": positions / t_cold, "logits_GBps": bytes_ / t_cold / 1e9,
@@ -226,12 +226,13 @@ def _row(name, shape, sel, positions, bytes_, t_cold, t_hot, stream_gbps, extra=
     return d
 
 
-def per_config_report(fd, torch, workloads, dev, stream_gbps, reps):
+def per_workload_report(fd, torch, workloads, dev, stream_gbps, reps):
     import gc
     rows = []
     scratch = torch.empty(512 << 20, dtype=torch.uint8, device=dev)
     sels = {k: [(s, p) for s in v["selectors"] for p in v["params"][s]]
-            for k, v in workloads.CONFIGS.items()}
+            for k, v in workloads.RECIPES.items()}
+    name = workloads.RECIPE_NAMES
 
     def static(k, inp, label, cold_needed=True):
         B, L, V = inp.logits.shape
@@ -243,21 +244,21 @@ def per_config_report(fd, torch, workloads, dev, stream_gbps, reps):
             extra = {"mean_commits_per_block": commits}
             if not cold_needed:
                 extra["note"] = "cold by size: the step reads far more than the caches hold"
-            rows.append(_row(k, label, f"{sel}({p})", pos, nbytes, tc, th, stream_gbps, extra))
-            log(f"config{k} {sel}({p}): {1e3 * tc:.3f} ms cold, {nbytes / tc / 1e9:.0f} GB/s")
+            rows.append(_row(name[k], label, f"{sel}({p})", pos, nbytes, tc, th, stream_gbps, extra))
+            log(f"{name[k]} {sel}({p}): {1e3 * tc:.3f} ms cold, {nbytes / tc / 1e9:.0f} GB/s")
 
-    log("per-config: config1")
-    inp = workloads.config1(device=dev)
-    static(1, inp, "B=1 L=32 V=126464 fp32")
+    log("per-workload: single block")
+    inp = workloads.single_block_b1_l32(device=dev)
+    static(workloads.SINGLE_BLOCK, inp, "B=1 L=32 V=126464 fp32")
     del inp
-    log("per-config: config3")
-    inp = workloads.config3(device=dev)
-    static(3, inp, "B=64 span 512, m_b~U{1..32}, V=126464 bf16")
+    log("per-workload: sparse blocks")
+    inp = workloads.sparse_b64_g512(device=dev)
+    static(workloads.SPARSE_BLOCKS, inp, "B=64 span 512, m_b~U{1..32}, V=126464 bf16")
     del inp
     gc.collect()
     torch.cuda.empty_cache()
-    # config2: whole simulated generations, one per selector
-    for sel, p in sels[2]:
+    # whole simulated generations (B=8 of 256), one per selector
+    for sel, p in sels[workloads.GENERATION]:
         gen = workloads.SimulatedGeneration(2, device=dev)
         nc = torch.empty((gen.B,), dtype=torch.int32, device=dev)
         steps, commits, positions, ktime, ws = 0, 0, 0, 0.0, None
@@ -278,7 +279,7 @@ def per_config_report(fd, torch, workloads, dev, stream_gbps, reps):
                          f"{sel}({p})", positions / steps, nbytes / steps, ktime / steps, None,
                          stream_gbps, {"steps": steps, "commits_per_step": commits / steps,
                                        "note": "hot: each step's rows were just written"}))
-        log(f"config2 {sel}({p}): {steps} steps, {commits / steps:.2f} commits/step")
+        log(f"generation_b8_g256 {sel}({p}): {steps} steps, {commits / steps:.2f} commits/step")
         del gen
     gc.collect()
     torch.cuda.empty_cache()
@@ -298,7 +299,7 @@ def per_config_report(fd, torch, workloads, dev, stream_gbps, reps):
             steps = gen.run()
             walls.append(time.perf_counter() - t0)
         w = sorted(walls)[len(walls) // 2]
-        rows.append({"config": "2-loop", "shape": f"B=8 gen 256 in blocks of 32, V={V_loop} bf16",
+        rows.append({"workload": "device-loop", "shape": f"B=8 gen 256 in blocks of 32, V={V_loop} bf16",
                      "selector": "profile(1.0)", "mode": mode, "steps": steps,
                      "ms_per_generation": 1e3 * w, "us_per_step": 1e6 * w / steps,
                      "tokens_per_s": 8 * 256 / w})
@@ -344,7 +345,7 @@ def per_config_report(fd, torch, workloads, dev, stream_gbps, reps):
             tp.append(e2.elapsed_time(e3) * 1e-3 / burst)
         med = lambda v: sorted(v)[len(v) // 2]
         flops = 2.0 * B_lm * L_lm * d_model * workloads.V_LLADA
-        rows.append({"config": "lmhead", "shape": f"{B_lm * L_lm} positions, d={d_model}, V={workloads.V_LLADA}",
+        rows.append({"workload": "lmhead", "shape": f"{B_lm * L_lm} positions, d={d_model}, V={workloads.V_LLADA}",
                      "fused_ms": 1e3 * med(tf), "fused_TFLOPs": flops / med(tf) / 1e12,
                      "frac_of_bf16_peak": flops / med(tf) / 2.5e15,
                      "unfused_gemm_ms": 1e3 * med(tg), "unfused_pass_ms": 1e3 * med(tp),
@@ -356,10 +357,10 @@ def per_config_report(fd, torch, workloads, dev, stream_gbps, reps):
     del weight
     gc.collect()
     torch.cuda.empty_cache()
-    log("per-config: config4 (first step of the generation)")
-    gen = workloads.SimulatedGeneration(4, device=dev)
+    log("per-workload: bimodal generation (its first step)")
+    gen = workloads.SimulatedGeneration(workloads.BIMODAL_GENERATION, device=dev)
     inp = gen.prepare_step()
-    static(4, inp, "B=256 span 1024 (66 GB allocated), block 64, V=126464 bf16", cold_needed=False)
+    static(workloads.BIMODAL_GENERATION, inp, "B=256 span 1024 (66 GB allocated), block 64, V=126464 bf16", cold_needed=False)
     del inp, gen
     gc.collect()
     torch.cuda.empty_cache()
@@ -367,26 +368,26 @@ def per_config_report(fd, torch, workloads, dev, stream_gbps, reps):
     return rows
 
 
-def per_config_markdown(rows, c5, stream_gbps, cmd) -> str:
+def per_workload_markdown(rows, stress, stream_gbps, cmd) -> str:
     out = ["# Decode-step throughput per workload recipe (one MI355X)", "",
            "Command (from the repository root):", "", f"    {cmd}", "",
            f"Read-only stream reference (`fdllm_stream_read` over the 8.29 GB logits buffer): "
            f"{stream_gbps:.0f} GB/s.  Kernel times are HIP-event averages of `fdllm_decode_step`; "
            "`cold` overwrites a 512 MB buffer before every step (evicting L2 and the Infinity "
-           "Cache), `hot` does not.  The per-step traffic of config2 is 8x32 rows, so its steps "
+           "Cache), `hot` does not.  The per-step traffic of the B=8 generation is 8x32 rows, so its steps "
            "are launch-bound.", "",
-           "| config | shape | selector | positions/step | kernel ms (cold) | kernel ms (hot) | "
+           "| workload | shape | selector | positions/step | kernel ms (cold) | kernel ms (hot) | "
            "positions/s | logits GB/s | % of 8 TB/s | % of stream | commits |",
            "|---|---|---|---|---|---|---|---|---|---|---|"]
-    loop = [r for r in rows if r["config"] == "2-loop"]
-    lm = [r for r in rows if r["config"] == "lmhead"]
-    rows = [r for r in rows if r["config"] not in ("2-loop", "lmhead")]
-    for r in rows + c5:
+    loop = [r for r in rows if r["workload"] == "device-loop"]
+    lm = [r for r in rows if r["workload"] == "lmhead"]
+    rows = [r for r in rows if r["workload"] not in ("device-loop", "lmhead")]
+    for r in rows + stress:
         hot = f"{r['kernel_ms_hot']:.4f}" if r["kernel_ms_hot"] is not None else "—"
         commits = (f"{r['commits_per_step']:.2f}/step, {r['steps']} steps" if "steps" in r
                    else f"{r.get('mean_commits_per_block', 0):.2f}/block")
         fs = f"{100 * r['frac_of_stream']:.1f}" if r["frac_of_stream"] else "—"
-        out.append(f"| {r['config']} | {r['shape']} | {r['selector']} | {r['positions_per_step']:.0f} | "
+        out.append(f"| {r['workload']} | {r['shape']} | {r['selector']} | {r['positions_per_step']:.0f} | "
                    f"{r['kernel_ms_cold']:.4f} | {hot} | {r['positions_per_s']:.4g} | "
                    f"{r['logits_GBps']:.0f} | {100 * r['frac_of_peak']:.1f} | {fs} | {commits} |")
     if loop:
@@ -426,8 +427,8 @@ def main():
     ap.add_argument("--cpu-worker-blocks", type=int, default=60, help="blocks per oracle process")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-selector-sweep", action="store_true")
-    ap.add_argument("--per-config", action="store_true", help="also time the other workload recipes")
-    ap.add_argument("--per-config-md", default=None, help="write the per-config table here")
+    ap.add_argument("--per-workload", action="store_true", help="also time the other workload recipes")
+    ap.add_argument("--per-workload-md", default=None, help="write the per-workload table here")
     ap.add_argument("--copy-calibration-mb", type=int, default=1024,
                     help="size of a plain device copy timed (and counted by rocprofv3) for reference")
     args = ap.parse_args()
@@ -457,8 +458,8 @@ def main():
     fd.load()
     dev = torch.device("cuda", 0)
     torch.cuda.set_device(dev)
-    log(f"generating config5 inputs on {torch.cuda.get_device_name(dev)}")
-    inp = workloads.config5(device=dev, progress=log)
+    log(f"generating the throughput-stress inputs on {torch.cuda.get_device_name(dev)}")
+    inp = workloads.stress_b1024_l32(device=dev, progress=log)
     B, L, V = inp.logits.shape
     positions = int(inp.mask.sum())
     logits_bytes = positions * V * inp.logits.element_size()
@@ -536,7 +537,7 @@ def main():
     wall, kavg, kmin = run(args.selector, param, args.steps, args.warmup, f"{args.selector}({param})")
     commits = float(outs["n_commit"].float().mean())
     sweep = {}
-    c5_rows = [_row(5, "B=1024 L=32 V=126464 bf16", f"{args.selector}({param})", positions,
+    stress_rows = [_row(workloads.RECIPE_NAMES[workloads.STRESS], "B=1024 L=32 V=126464 bf16", f"{args.selector}({param})", positions,
                     logits_bytes, kavg, None, stream_gbps, {"mean_commits_per_block": commits})]
     if not args.no_selector_sweep:
         for sel, p in [("profile", 1.0), ("profile", 0.75), ("factor", 1.0), ("factor", 0.75),
@@ -548,7 +549,7 @@ def main():
             mc = float(outs["n_commit"].float().mean())
             sweep[f"{sel}({p})"] = {"ms_per_step": 1e3 * w2 / n2, "kernel_ms": 1e3 * k2,
                                     "mean_commits_per_block": mc}
-            c5_rows.append(_row(5, "B=1024 L=32 V=126464 bf16", f"{sel}({p})", positions,
+            stress_rows.append(_row(workloads.RECIPE_NAMES[workloads.STRESS], "B=1024 L=32 V=126464 bf16", f"{sel}({p})", positions,
                                 logits_bytes, k2, None, stream_gbps, {"mean_commits_per_block": mc}))
     ms = 1e3 * wall / args.steps
     value = positions * args.steps / wall
@@ -567,7 +568,7 @@ def main():
         "vs_baseline": None,
         "dtype": "f32",
         "data": "synthetic",
-        "config": {"workload": "config5 throughput stress: B=1024 blocks x L=32 masked positions, "
+        "config": {"workload": "throughput stress: B=1024 blocks x L=32 masked positions, "
                                "V=126464 bf16 logits (Gumbel(0,1), 10% planted near-ties), one fused "
                                f"decode step ({args.selector} {'tau' if args.selector == 'threshold' else 'f'}={param})",
                    "B": B, "L": L, "V": V, "logits_dtype": "bf16", "selector": args.selector,
@@ -588,13 +589,13 @@ def main():
         "copy_reference": copy_ref,
         "source_sha256_16": source_digest(),
     }
-    if args.per_config:
-        rows = per_config_report(fd, torch, workloads, dev, stream_gbps, reps=10)
-        line["per_config"] = rows + c5_rows
-        if args.per_config_md:
+    if args.per_workload:
+        rows = per_workload_report(fd, torch, workloads, dev, stream_gbps, reps=10)
+        line["per_workload"] = rows + stress_rows
+        if args.per_workload_md:
             cmd = "python bench.py " + " ".join(sys.argv[1:])
-            with open(args.per_config_md, "w") as fh:
-                fh.write(per_config_markdown(rows, c5_rows, stream_gbps, cmd))
+            with open(args.per_workload_md, "w") as fh:
+                fh.write(per_workload_markdown(rows, stress_rows, stream_gbps, cmd))
     if not args.no_cpu_baseline:
         log(f"cpu_baseline: oracle on {args.cpu_blocks} blocks, one core")
         single = cpu_baseline_single(inp, args.cpu_blocks, args.selector, param)

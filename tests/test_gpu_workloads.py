@@ -1,9 +1,9 @@
 """GPU parity on the five workload recipes at their full sizes.
 
-Configs 1 and 3 are checked on every candidate row; config 5 (8.3 GB of
-logits) on a seeded sample of blocks plus properties that hold at any size;
-the simulated generations (configs 2 and 4) run in lockstep with the oracle
-for their first steps.
+The single-block and sparse-block recipes are checked on every candidate
+row; the throughput stress (8.3 GB of logits) on a seeded sample of blocks
+plus properties that hold at any size; the simulated generations run in
+lockstep with the oracle for their first steps.
 """
 import gc
 
@@ -59,9 +59,9 @@ def _check_step(inp, o, bs, rule, p):
     return nf, nfm, worst, r
 
 
-def test_config1_full(gpu):
-    say("[config1] B=1 L=32 V=126464 fp32")
-    inp = workloads.config1(device="cuda")
+def test_single_block_b1_l32_full(gpu):
+    say("[single block] B=1 L=32 V=126464 fp32")
+    inp = workloads.single_block_b1_l32(device="cuda")
     for rule, p in [("profile", 1.0), ("factor", 1.0), ("threshold", 0.9)]:
         mask, x, o = _decode(gpu, inp, rule, p)
         nf, nfm, worst, r = _check_step(inp, o, [0], rule, p)
@@ -74,9 +74,9 @@ def test_config1_full(gpu):
         assert tok[i] == int(np.argmax(rows[i]))
 
 
-def test_config3_full(gpu):
-    say("[config3] B=64 L=512 V=126464 bf16, poisoned non-candidate rows")
-    inp = workloads.config3(device="cuda")
+def test_sparse_b64_g512_full(gpu):
+    say("[sparse blocks] B=64 L=512 V=126464 bf16, poisoned non-candidate rows")
+    inp = workloads.sparse_b64_g512(device="cuda")
     g = gpu_confidence(gpu, inp)
     assert all(bool(torch.isfinite(t.float()).all()) for t in g[1:])
     for rule, p in [("profile", 1.0), ("profile", 0.75), ("factor", 1.0), ("factor", 0.75),
@@ -98,9 +98,9 @@ def test_config3_full(gpu):
     _free()
 
 
-def test_config5_sampled(gpu):
-    say("[config5] B=1024 L=32 V=126464 bf16 (8.3 GB), fused decode step")
-    inp = workloads.config5(device="cuda")
+def test_stress_b1024_l32_sampled(gpu):
+    say("[throughput stress] B=1024 L=32 V=126464 bf16 (8.3 GB), fused decode step")
+    inp = workloads.stress_b1024_l32(device="cuda")
     B, L, V = inp.logits.shape
     rng = np.random.default_rng(2026)
     sample = sorted(rng.choice(B, 24, replace=False).tolist())
@@ -145,8 +145,8 @@ def test_config5_sampled(gpu):
     _free()
 
 
-def _simulate(gpu, config, rules, steps, check_bs, B=None):
-    sim = workloads.SimulatedGeneration(config, device="cuda", B=B)
+def _simulate(gpu, recipe, rules, steps, check_bs, B=None):
+    sim = workloads.SimulatedGeneration(recipe, device="cuda", B=B)
     flagged_total = 0
     for s in range(steps):
         if sim.done():
@@ -183,23 +183,23 @@ def _sub_mask(inp, bs):
     return m
 
 
-def test_config2_simulation(gpu):
-    say("[config2] B=8 gen 256 in blocks of 32, lockstep with the oracle")
+def test_generation_b8_g256_simulation(gpu):
+    say("[generation] B=8 gen 256 in blocks of 32, lockstep with the oracle")
     rules = [("profile", 1.0), ("factor", 1.0), ("profile", 0.5), ("factor", 0.5),
              ("profile", 2.0), ("factor", 2.0), ("threshold", 0.9)]
-    for sim, inp, outs in _simulate(gpu, 2, rules, steps=6, check_bs=range(8)):
+    for sim, inp, outs in _simulate(gpu, workloads.GENERATION, rules, steps=6, check_bs=range(8)):
         for f in (0.5, 1.0, 2.0):
             assert (outs[("profile", f)][2]["n_commit"] >= outs[("factor", f)][2]["n_commit"]).all()
     _free()
 
 
-def test_config4_simulation(gpu):
-    say("[config4] B=256 gen 1024 in blocks of 64, lockstep on a subset incl. all flat sequences")
-    sim_probe = workloads.SimulatedGeneration(4, device="cpu", V=8)
+def test_bimodal_b256_g1024_simulation(gpu):
+    say("[bimodal generation] B=256 gen 1024 in blocks of 64, lockstep on a subset incl. all flat sequences")
+    sim_probe = workloads.SimulatedGeneration(workloads.BIMODAL_GENERATION, device="cpu", V=8)
     flat = [b for b in range(256) if sim_probe.flat[b]]
     check = sorted(set(flat) | {0, 1, 100, 255})
     rules = [("profile", 1.0), ("factor", 1.0), ("profile", 0.75), ("factor", 0.75), ("threshold", 0.9)]
-    for sim, inp, outs in _simulate(gpu, 4, rules, steps=2, check_bs=check):
+    for sim, inp, outs in _simulate(gpu, workloads.BIMODAL_GENERATION, rules, steps=2, check_bs=check):
         for f in (0.75, 1.0):
             npf = outs[("profile", f)][2]["n_commit"].cpu().numpy()
             nfa = outs[("factor", f)][2]["n_commit"].cpu().numpy()

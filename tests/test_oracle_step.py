@@ -108,8 +108,8 @@ def test_workload_shapes_small():
             assert bool(torch.isfinite(inp.logits[b, i].float()).all()) == bool(cand)
 
 
-def test_config1_recipe():
-    inp = workloads.config1(V=4096)
+def test_single_block_recipe():
+    inp = workloads.single_block_b1_l32(V=4096)
     lg = inp.logits[0].double().numpy()
     # exactly two rows carry an exact tie at the maximum
     ties = sum(int((row == row.max()).sum() >= 2) for row in lg)

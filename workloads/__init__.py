@@ -13,7 +13,7 @@ paper's decoding geometry: block size 32 (Table 1 caption), generation lengths
 operating points tau=0.9, f=0.75/1.0, delta=0.25 (Sec. 5, "Parameter
 selection"; Table 5).  The vocabulary size V=126464 is LLaDA's.
 
-Every draw comes from a ``torch.Generator`` seeded by ``seed_for(config,
+Every draw comes from a ``torch.Generator`` seeded by ``seed_for(recipe,
 step, b)``, so a sequence's logits at a step are reproducible on the same
 device type.  CPU and GPU generators produce different streams: a parity
 check always hands the oracle a host copy of the exact tensor the GPU read.
@@ -34,13 +34,23 @@ import torch
 
 V_LLADA = 126464          # LLaDA-8B vocabulary
 MASK_ID = -1              # token id stored in x for a still-masked position
-BASE_SEED = 20260601      # config k uses BASE_SEED + k
+BASE_SEED = 20260601      # recipe k draws from BASE_SEED + k
+
+# the seed salts of the five benchmark recipes
+SINGLE_BLOCK = 1          # B=1, one block of 32, fp32
+GENERATION = 2            # B=8, generation of 256 in blocks of 32
+SPARSE_BLOCKS = 3         # B=64, span 512, partly masked blocks of 32
+BIMODAL_GENERATION = 4    # B=256, generation of 1024 in blocks of 64
+STRESS = 5                # B=1024, L=32, all masked
+RECIPE_NAMES = {SINGLE_BLOCK: "single_block_b1_l32", GENERATION: "generation_b8_g256",
+                SPARSE_BLOCKS: "sparse_b64_g512", BIMODAL_GENERATION: "bimodal_b256_g1024",
+                STRESS: "stress_b1024_l32"}
 BF16_NAN = 0x7FC0         # poison for logits rows that must never be read
 
 
-def seed_for(config: int, step: int, b: int) -> int:
-    """Deterministic 63-bit seed for (config, step, sequence)."""
-    h = (BASE_SEED + config) * 0x9E3779B97F4A7C15
+def seed_for(recipe: int, step: int, b: int) -> int:
+    """Deterministic 63-bit seed for (recipe, step, sequence)."""
+    h = (BASE_SEED + recipe) * 0x9E3779B97F4A7C15
     h ^= (step + 1) * 0xBF58476D1CE4E5B9
     h ^= (b + 1) * 0x94D049BB133111EB
     h &= (1 << 64) - 1
@@ -48,9 +58,9 @@ def seed_for(config: int, step: int, b: int) -> int:
     return h & ((1 << 63) - 1)
 
 
-def _gen(config: int, step: int, b: int, device) -> torch.Generator:
+def _gen(recipe: int, step: int, b: int, device) -> torch.Generator:
     g = torch.Generator(device=device)
-    g.manual_seed(seed_for(config, step, b))
+    g.manual_seed(seed_for(recipe, step, b))
     return g
 
 
@@ -106,11 +116,11 @@ class StepInputs:
 
 
 # ---------------------------------------------------------------------------
-# config 1: B=1, one block of 32 all-masked positions, fp32, N(0,1)+U(0,12)
+# single block: B=1, one block of 32 all-masked positions, fp32, N(0,1)+U(0,12)
 # spike; 4 positions get a second spike (2 exact ties, 2 gaps in [1e-6,1e-3]).
 # ---------------------------------------------------------------------------
-def config1(device="cpu", V: int = V_LLADA, L: int = 32) -> StepInputs:
-    g = _gen(1, 0, 0, device)
+def single_block_b1_l32(device="cpu", V: int = V_LLADA, L: int = 32) -> StepInputs:
+    g = _gen(SINGLE_BLOCK, 0, 0, device)
     rows = torch.randn((L, V), generator=g, device=device, dtype=torch.float32)
     tok = _distinct_tokens(g, L, 2, V, device)
     h = _uniform(g, (L, 1), 0.0, 12.0, device)
@@ -130,18 +140,18 @@ def config1(device="cpu", V: int = V_LLADA, L: int = 32) -> StepInputs:
     start = torch.zeros((1,), dtype=torch.int32, device=device)
     end = torch.full((1,), L, dtype=torch.int32, device=device)
     x = torch.full((1, L), MASK_ID, dtype=torch.int32, device=device)
-    return StepInputs(logits, mask, start, end, x, "config1",
+    return StepInputs(logits, mask, start, end, x, "single_block_b1_l32",
                       "B=1 L=32 fp32 N(0,1)+U(0,12) spike, 2 exact ties + 2 near ties")
 
 
 # ---------------------------------------------------------------------------
-# config 2 / config 4: full simulated generations.  The whole generation span
+# generations (B=8 of 256, B=256 of 1024): full simulated generations.  The whole generation span
 # is one logits tensor [B, G, V] ("no-cache" layout); each step fills only the
 # rows of every sequence's active block, which start/end select.
 # ---------------------------------------------------------------------------
 @dataclasses.dataclass
 class Generation:
-    config: int
+    recipe: int
     B: int
     G: int                    # generation length
     blk: int                  # block size
@@ -188,22 +198,22 @@ class SimulatedGeneration:
     has a masked position).  Selection itself is not done here.
     """
 
-    def __init__(self, config: int, device="cpu", B=None, V: int = V_LLADA):
-        if config == 2:
+    def __init__(self, recipe: int, device="cpu", B=None, V: int = V_LLADA):
+        if recipe == GENERATION:
             self.B, self.G, self.blk = (B or 8), 256, 32
-        elif config == 4:
+        elif recipe == BIMODAL_GENERATION:
             self.B, self.G, self.blk = (B or 256), 1024, 64
         else:
-            raise ValueError("simulated generations are configs 2 and 4")
-        self.config, self.V, self.device = config, V, device
+            raise ValueError("simulated generations are GENERATION and BIMODAL_GENERATION")
+        self.recipe, self.V, self.device = recipe, V, device
         self.dtype = torch.bfloat16
-        g = _gen(config, 0, 10_000, device)
+        g = _gen(recipe, 0, 10_000, device)
         # per-(sequence, position) spike token, fixed for the whole generation
         self.tok = torch.randint(0, V, (self.B, self.G), generator=g, device=device)
-        if config == 4:
+        if recipe == BIMODAL_GENERATION:
             self.temp = _uniform(g, (self.B,), 0.5, 2.0, device).tolist()
             self.flat = torch.zeros(self.B, dtype=torch.bool)
-            self.flat[torch.randperm(self.B, generator=torch.Generator().manual_seed(seed_for(4, 0, 0)))[:16 * self.B // 256 or 1]] = True
+            self.flat[torch.randperm(self.B, generator=torch.Generator().manual_seed(seed_for(BIMODAL_GENERATION, 0, 0)))[:16 * self.B // 256 or 1]] = True
             for b in range(self.B):
                 if self.flat[b]:
                     self.temp[b] = 1.0
@@ -236,10 +246,10 @@ class SimulatedGeneration:
                 continue                      # finished: empty window
             lo, hi = k * self.blk, (k + 1) * self.blk
             s[b], e[b] = lo, hi
-            g = _gen(self.config, self.step_no, b, self.device)
+            g = _gen(self.recipe, self.step_no, b, self.device)
             rows = torch.empty((self.blk, self.V), dtype=torch.float32, device=self.device)
             pos = torch.arange(lo, hi, device=self.device)
-            if self.config == 2:
+            if self.recipe == GENERATION:
                 _c2_fill(rows, b, self.step_no, pos, self.tok[b], g, self.device)
             else:
                 _c4_fill(rows, b, self.step_no, pos, self.tok[b], g, self.device,
@@ -249,17 +259,17 @@ class SimulatedGeneration:
         self.end.copy_(e)
         self.step_no += 1
         return StepInputs(self.logits, self.mask, self.start, self.end, self.x,
-                          f"config{self.config}-step{self.step_no - 1}")
+                          f"{RECIPE_NAMES[self.recipe]}-step{self.step_no - 1}")
 
 
 # ---------------------------------------------------------------------------
-# config 3: B=64, gen 512 in blocks of 32, no-cache layout [64,512,V] bf16;
+# sparse blocks: B=64, gen 512 in blocks of 32, no-cache layout [64,512,V] bf16;
 # sequence b is at a seeded block k_b with m_b ~ U{1..32} masked positions.
 # Background N(0, sd=2) plus Zipf(1.1)-ranked spikes on 5 tokens.
 # ---------------------------------------------------------------------------
-def config3(device="cpu", V: int = V_LLADA, B: int = 64, G: int = 512, blk: int = 32,
+def sparse_b64_g512(device="cpu", V: int = V_LLADA, B: int = 64, G: int = 512, blk: int = 32,
             poison: bool = True) -> StepInputs:
-    g0 = _gen(3, 0, 10_000, device)
+    g0 = _gen(SPARSE_BLOCKS, 0, 10_000, device)
     k = torch.randint(0, G // blk, (B,), generator=g0, device="cpu" if device == "cpu" else device).cpu()
     m = torch.randint(1, blk + 1, (B,), generator=g0, device="cpu" if device == "cpu" else device).cpu()
     logits = torch.empty((B, G, V), dtype=torch.bfloat16, device=device)
@@ -269,7 +279,7 @@ def config3(device="cpu", V: int = V_LLADA, B: int = 64, G: int = 512, blk: int 
     x = torch.randint(0, V, (B, G), generator=g0, device=device).to(torch.int32)
     ranks = torch.arange(1, 6, device=device, dtype=torch.float32)
     for b in range(B):
-        g = _gen(3, 0, b, device)
+        g = _gen(SPARSE_BLOCKS, 0, b, device)
         lo = int(k[b]) * blk
         sel = torch.randperm(blk, generator=g, device=device)[: int(m[b])] + lo
         mask[b, sel] = 1
@@ -282,17 +292,17 @@ def config3(device="cpu", V: int = V_LLADA, B: int = 64, G: int = 512, blk: int 
         logits[b, sel] = rows.to(torch.bfloat16)
     start = (k * blk).to(torch.int32).to(device)
     end = ((k + 1) * blk).to(torch.int32).to(device)
-    return StepInputs(logits, mask, start, end, x, "config3",
+    return StepInputs(logits, mask, start, end, x, "sparse_b64_g512",
                       "B=64 no-cache [64,512,V] bf16, m_b~U{1..32}, N(0,2)+Zipf(1.1) top-5 spikes")
 
 
 # ---------------------------------------------------------------------------
-# config 5: throughput stress. B=1024, L=32, all masked, bf16 Gumbel(0,1)
+# throughput stress: B=1024, L=32, all masked, bf16 Gumbel(0,1)
 # background; 10% of positions carry a planted pair with gap U(0,1e-3).
 # ---------------------------------------------------------------------------
-def config5_rows(b: int, device="cpu", V: int = V_LLADA, L: int = 32) -> torch.Tensor:
+def stress_b1024_l32_rows(b: int, device="cpu", V: int = V_LLADA, L: int = 32) -> torch.Tensor:
     """The [L, V] bf16 logits of sequence b (its own seeded stream per device)."""
-    g = _gen(5, 0, b, device)
+    g = _gen(STRESS, 0, b, device)
     rows = _gumbel(g, (L, V), device)
     tie = torch.rand((L,), generator=g, device=device) < 0.10
     toks = _distinct_tokens(g, L, 2, V, device)
@@ -305,19 +315,19 @@ def config5_rows(b: int, device="cpu", V: int = V_LLADA, L: int = 32) -> torch.T
     return rows.to(torch.bfloat16)
 
 
-def config5(device="cpu", V: int = V_LLADA, B: int = 1024, L: int = 32,
+def stress_b1024_l32(device="cpu", V: int = V_LLADA, B: int = 1024, L: int = 32,
             chunk: int = 32, progress: Optional[Callable[[str], None]] = None) -> StepInputs:
     logits = torch.empty((B, L, V), dtype=torch.bfloat16, device=device)
     for b0 in range(0, B, chunk):
         if progress is not None and b0 % 256 == 0:
-            progress(f"config5 inputs: sequences {b0}..{min(B, b0 + 256) - 1}")
+            progress(f"stress inputs: sequences {b0}..{min(B, b0 + 256) - 1}")
         for b in range(b0, min(B, b0 + chunk)):
-            logits[b] = config5_rows(b, device, V, L)
+            logits[b] = stress_b1024_l32_rows(b, device, V, L)
     mask = torch.ones((B, L), dtype=torch.uint8, device=device)
     start = torch.zeros((B,), dtype=torch.int32, device=device)
     end = torch.full((B,), L, dtype=torch.int32, device=device)
     x = torch.full((B, L), MASK_ID, dtype=torch.int32, device=device)
-    return StepInputs(logits, mask, start, end, x, "config5",
+    return StepInputs(logits, mask, start, end, x, "stress_b1024_l32",
                       "B=1024 L=32 bf16 Gumbel(0,1), 10% planted near-ties gap<1e-3")
 
 
@@ -365,19 +375,19 @@ def random_case(B: int, L: int, V: int, dtype=torch.bfloat16, device="cpu", seed
                       f"random(B={B},L={L},V={V},{str(dtype).split('.')[-1]},seed={seed})")
 
 
-CONFIGS = {
-    1: dict(B=1, L=32, V=V_LLADA, dtype="f32", selectors=["profile", "factor", "threshold"],
+RECIPES = {
+    SINGLE_BLOCK: dict(B=1, L=32, V=V_LLADA, dtype="f32", selectors=["profile", "factor", "threshold"],
             params=dict(profile=[1.0], factor=[1.0], threshold=[0.9])),
-    2: dict(B=8, L=256, V=V_LLADA, dtype="bf16", block=32,
+    GENERATION: dict(B=8, L=256, V=V_LLADA, dtype="bf16", block=32,
             selectors=["profile", "factor", "threshold"],
             params=dict(profile=[0.5, 1.0, 2.0], factor=[0.5, 1.0, 2.0], threshold=[0.9])),
-    3: dict(B=64, L=512, V=V_LLADA, dtype="bf16", block=32,
+    SPARSE_BLOCKS: dict(B=64, L=512, V=V_LLADA, dtype="bf16", block=32,
             selectors=["profile", "factor", "threshold"],
             params=dict(profile=[1.0, 0.75], factor=[1.0, 0.75], threshold=[0.9])),
-    4: dict(B=256, L=1024, V=V_LLADA, dtype="bf16", block=64,
+    BIMODAL_GENERATION: dict(B=256, L=1024, V=V_LLADA, dtype="bf16", block=64,
             selectors=["profile", "factor", "threshold"],
             params=dict(profile=[0.75, 1.0], factor=[0.75, 1.0], threshold=[0.9])),
-    5: dict(B=1024, L=32, V=V_LLADA, dtype="bf16", selectors=["profile", "factor", "threshold"],
+    STRESS: dict(B=1024, L=32, V=V_LLADA, dtype="bf16", selectors=["profile", "factor", "threshold"],
             params=dict(profile=[1.0, 0.75], factor=[1.0, 0.75], threshold=[0.9])),
 }
 
