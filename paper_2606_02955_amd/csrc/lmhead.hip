@@ -82,13 +82,14 @@ struct LmState {
   int first;
 };
 
-// Folds the lane's 32 accumulators of one position (vocabulary entries
+// Folds the lane's accumulators of one position (vocabulary entries
 // base + 16 mi + i, increasing in (mi, i)) into its state.
-__device__ __forceinline__ void lm_fold(LmState& st, const f32x4 (&acc)[8][4], int ni, int base,
-                                          int V) {
+template <int MI, int NI>
+__device__ __forceinline__ void lm_fold(LmState& st, const f32x4 (&acc)[MI][NI], int ni, int base,
+                                        int V) {
   float tm = kNegInf;
 #pragma unroll
-  for (int mi = 0; mi < 8; ++mi)
+  for (int mi = 0; mi < MI; ++mi)
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       const int v = base + 16 * mi + i;
@@ -101,7 +102,7 @@ __device__ __forceinline__ void lm_fold(LmState& st, const f32x4 (&acc)[8][4], i
     st.M = tm;
     int f = 0x7fffffff;
 #pragma unroll
-    for (int mi = 7; mi >= 0; --mi)
+    for (int mi = MI - 1; mi >= 0; --mi)
 #pragma unroll
       for (int i = 3; i >= 0; --i) {
         const int v = base + 16 * mi + i;
@@ -113,7 +114,7 @@ __device__ __forceinline__ void lm_fold(LmState& st, const f32x4 (&acc)[8][4], i
   // stays exact and s' = (S - e_M) / e_M keeps its relative accuracy
   double sum[2] = {0.0, 0.0};
 #pragma unroll
-  for (int mi = 0; mi < 8; ++mi)
+  for (int mi = 0; mi < MI; ++mi)
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       const int v = base + 16 * mi + i;
@@ -365,7 +366,7 @@ k_lm_partial(const uint16_t* __restrict__ hidden, const uint16_t* __restrict__ w
     }
     const int base = t * kLmVt + 128 * vw + 4 * (lane / 16);
 #pragma unroll
-    for (int ni = 0; ni < 4; ++ni) lm_fold(st[ni], acc, ni, base, V);
+    for (int ni = 0; ni < 4; ++ni) lm_fold<8, 4>(st[ni], acc, ni, base, V);
   }
 #undef LM_M
   // lanes l, l^16, l^32, l^48 hold the same positions
@@ -402,6 +403,207 @@ k_lm_partial(const uint16_t* __restrict__ hidden, const uint16_t* __restrict__ w
   }
 }
 
+// ---------------------------------------------------------------------------
+// at most kLsRows positions in all (one sequence's block)
+// ---------------------------------------------------------------------------
+// With few positions the LM head is bound by reading W once (2 V d bytes;
+// the 2 N V d flop are a few percent of the matrix cores' time), and the rate
+// of that read depends on how it is issued: streams that each read a few rows
+// 8 KiB apart reach ~5 TB/s, a contiguous range per workgroup read by global
+// loads ~7 TB/s, the same range by buffer_load ... lds ~6.2 TB/s.  Here every
+// workgroup streams a contiguous range of W, kLsBlk whole rows (16 d bytes)
+// per block: each wave load instruction reads 1 KiB in address order into
+// registers, which are stored to LDS while the next block's loads are in
+// flight.
+// The 8 waves split the hidden dimension and keep their share of the
+// positions' hidden operands in registers for the whole kernel; per block each
+// wave runs its MFMAs over its share (A = the block's rows from LDS, B = the
+// hidden operands), and 256 threads each sum one (row, position) logit over
+// the 8 partial products and fold it into their own running state; the 8 row
+// states of a position are combined at the end.  Every workgroup finds the
+// candidate positions itself (there are at most 32); workgroup 0 also writes
+// them out, with their count, for the finish, and the default outputs of the
+// other positions.
+constexpr int kLsRows = 32;        // positions served (two 16-column MFMA blocks)
+constexpr int kLsWaves = 8;
+constexpr int kLsBlk = 8;          // vocabulary rows per block
+constexpr int kLsMaxD = 4096;      // hidden operands held in registers: d / 8 per wave
+// two row blocks and the waves' partial products (144 KiB at d = 4096)
+constexpr size_t kLsLdsBytes(int d) {
+  return 2 * (size_t)kLsBlk * d * 2 + (size_t)kLsWaves * 2 * kWave * sizeof(f32x4);
+}
+
+__device__ __forceinline__ int ls_swz(int r) { return r & 7; }
+
+// DM = d / 512: 16-byte loads per thread and block; 2 DM 32-element chunks
+// of the hidden dimension per wave
+template <int DM>
+__global__ void __launch_bounds__(kLsWaves * kWave)
+k_lm_stream(const uint16_t* __restrict__ hidden, const uint16_t* __restrict__ weight,
+            const uint8_t* __restrict__ mask, const int32_t* __restrict__ bstart,
+            const int32_t* __restrict__ bend, int B, int L, int V, int32_t* __restrict__ rows,
+            int32_t* __restrict__ count, RowOut out, WavePartial* __restrict__ partials,
+            int n_split) {
+  constexpr int d = DM * 512;
+  constexpr int NC = 2 * DM;                                 // 32-element chunks per wave
+  constexpr int vec_row = d / 8;                             // 16-byte vectors per row
+  constexpr uint32_t blk_bytes = (uint32_t)kLsBlk * d * 2;
+  extern __shared__ __attribute__((aligned(1024))) char ls_lds[];
+  __shared__ int32_t cand_rows[kLsRows];
+  __shared__ int cand_n;
+  const int t = threadIdx.x;
+  const int lane = t % kWave;
+  const int wave = __builtin_amdgcn_readfirstlane(t / kWave);
+  const int g = blockIdx.x;
+  const int G = gridDim.x;
+
+  // the candidate positions, in position order (B L <= kLsRows)
+  if (wave == 0) {
+    const int n = B * L;
+    bool cand = false;
+    if (lane < n) {
+      const int b = lane / L, q = lane % L;
+      const int s = bstart[b], e = bend[b];
+      cand = window_ok(s, e, L) && q >= s && q < e && mask[lane] != 0;
+    }
+    const unsigned long long bal = __ballot(cand);
+    const int idx = __popcll(bal & ((1ull << lane) - 1ull));
+    if (cand) cand_rows[idx] = lane;
+    if (lane == 0) cand_n = __popcll(bal);
+    if (g == 0) {
+      if (cand) rows[idx] = lane;
+      else if (lane < n) store_default(out, lane);
+      if (lane == 0) *count = __popcll(bal);
+    }
+  }
+  __syncthreads();
+  const int nrows = cand_n;
+  if (nrows == 0) return;
+
+  const int nblk = (V + kLsBlk - 1) / kLsBlk;
+  const int b_beg = (int)((long long)g * nblk / G), b_end = (int)((long long)(g + 1) * nblk / G);
+  const int cnt = b_end - b_beg;
+  float* red = reinterpret_cast<float*>(ls_lds + 2 * blk_bytes);  // f32x4 [wave][ni][lane]
+  const int k0 = wave * (d / kLsWaves);
+
+  // the hidden operands of this wave's share, for positions 16 ni + l % 16
+  // (past the count: the first row; their results are not stored)
+  u32x4 hb[NC][2];
+  {
+    const int q0 = lane % 16, q1 = 16 + lane % 16;
+    const uint16_t* h0 = hidden + (size_t)cand_rows[q0 < nrows ? q0 : 0] * d + k0 + 8 * (lane / 16);
+    const uint16_t* h1 = hidden + (size_t)cand_rows[q1 < nrows ? q1 : 0] * d + k0 + 8 * (lane / 16);
+#pragma unroll
+    for (int c = 0; c < NC; ++c) {
+      hb[c][0] = *reinterpret_cast<const u32x4*>(h0 + 32 * c);
+      hb[c][1] = *reinterpret_cast<const u32x4*>(h1 + 32 * c);
+    }
+  }
+  // block loads: thread t loads the block's 16-byte vectors j * 512 + t into
+  // registers (each wave instruction reads 1 KiB of W in address order) and
+  // stores them to LDS slot (row r, vector s ^ ls_swz(r)): the rows are 2 d
+  // bytes apart, a multiple of the bank period, and the swizzle puts the
+  // operand reads of the 8 rows in distinct banks.
+  const u32x4* wv = reinterpret_cast<const u32x4*>(weight);
+  u32x4 stg[DM];
+  auto load_regs = [&](int i) {
+    const int vb = (b_beg + i) * kLsBlk;
+#pragma unroll
+    for (int j = 0; j < DM; ++j) {
+      const int slot = j * kLsWaves * kWave + t;
+      const int v = min(vb + slot / vec_row, V - 1);         // rows past V repeat the last
+      stg[j] = __builtin_nontemporal_load(wv + (size_t)v * vec_row + slot % vec_row);
+    }
+  };
+  auto store_lds = [&](int buf) {
+    u32x4* bl = reinterpret_cast<u32x4*>(ls_lds + buf * blk_bytes);
+#pragma unroll
+    for (int j = 0; j < DM; ++j) {
+      const int slot = j * kLsWaves * kWave + t;
+      const int r = slot / vec_row, sv = slot % vec_row;
+      bl[r * vec_row + (sv ^ ls_swz(r))] = stg[j];
+    }
+  };
+  // the (row, position) of this thread's running state: threads 0..255 take
+  // row fr = t / 32 of every block and position fp = t % 32
+  const int fr = t / kLsRows, fp = t % kLsRows;
+  const bool folds = t < kLsBlk * kLsRows;
+  // where the logit of (fr, fp) sits among the waves' accumulators:
+  // ni = fp / 16, lane 16 (fr / 4) + fp % 16, element fr % 4
+  const int red_idx = ((fp / 16) * kWave + 16 * (fr / 4) + fp % 16) * 4 + fr % 4;
+  LmState st{kNegInf, kRefFloor, 0.0, 0x7fffffff};
+  // operand address of this lane in a buffer: row l % 8 (rows 8..15 of the
+  // MFMA block repeat rows 0..7), vector k0 / 8 + 4 c + l / 16
+  const int ar = lane % kLsBlk;
+  const int a_row = ar * vec_row;
+
+  load_regs(0);
+  store_lds(0);
+  // vmcnt(0): the hidden operands have arrived before the loop, so inside it
+  // the only loads in flight are the next block's, waited for at its store
+  // (without this the loop would wait for every load at its first MFMAs)
+  __builtin_amdgcn_s_waitcnt(0x0f70);
+  if (cnt > 1) load_regs(1);
+  for (int it = 0; it < cnt; ++it) {
+    const int buf = it & 1;
+    // the block is in LDS, and every thread has folded the previous block's
+    // logits (the partial products may be overwritten)
+    __syncthreads();
+    const u32x4* bl = reinterpret_cast<const u32x4*>(ls_lds + buf * blk_bytes);
+    f32x4 acc[2];
+#pragma unroll
+    for (int ni = 0; ni < 2; ++ni)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) acc[ni][i] = 0.0f;
+#pragma unroll
+    for (int c = 0; c < NC; ++c) {
+      const int sv = k0 / 8 + 4 * c + lane / 16;
+      const bf16x8 a = __builtin_bit_cast(bf16x8, bl[a_row + (sv ^ ls_swz(ar))]);
+#pragma unroll
+      for (int ni = 0; ni < 2; ++ni)
+        acc[ni] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, __builtin_bit_cast(bf16x8, hb[c][ni]),
+                                                          acc[ni], 0, 0, 0);
+    }
+    f32x4* redv = reinterpret_cast<f32x4*>(red);
+#pragma unroll
+    for (int ni = 0; ni < 2; ++ni) redv[(wave * 2 + ni) * kWave + lane] = acc[ni];
+    __syncthreads();
+    const int v = (b_beg + it) * kLsBlk + fr;
+    if (folds && v < V) {
+      float x = red[red_idx];
+#pragma unroll
+      for (int w = 1; w < kLsWaves; ++w) x += red[w * 2 * kWave * 4 + red_idx];
+      if (x > st.M) {
+        const float Kn = exp_ref(x);
+        st.S = rescale(st.S, st.K, Kn);
+        st.K = Kn;
+        st.M = x;
+        st.first = v;
+      }
+      st.S += (double)term(x, st.K);
+    }
+    // the next block into the buffer every wave finished reading before the
+    // barrier above, then the block after it into the registers
+    if (it + 1 < cnt) store_lds(buf ^ 1);
+    if (it + 2 < cnt) load_regs(it + 2);
+  }
+  // the row states of a position meet in LDS once every wave is done with
+  // the blocks
+  __syncthreads();
+  WavePartial* xs = reinterpret_cast<WavePartial*>(ls_lds);
+  if (folds) xs[fr * kLsRows + fp] = WavePartial{st.M, st.K, st.S, st.first};
+  __syncthreads();
+  if (t < kLsRows && t < nrows) {
+    LmState c = {xs[t].m, xs[t].K, xs[t].S, xs[t].first};
+#pragma unroll
+    for (int r = 1; r < kLsBlk; ++r) {
+      const WavePartial o = xs[r * kLsRows + t];
+      lm_combine(c, o.m, o.K, o.S, o.first);
+    }
+    partials[(size_t)t * n_split + g] = WavePartial{c.M, c.K, c.S, c.first};
+  }
+}
+
 // Per candidate row, one wavefront: lane l combines the splits l, l+64, ...
 // of the row's contiguous partials, then a fixed butterfly over the lanes
 // (both partners of every step form the same sum) and the finish.
@@ -434,16 +636,43 @@ k_lm_finish(const int32_t* __restrict__ rows, const int32_t* __restrict__ count,
 // ---------------------------------------------------------------------------
 constexpr int kLmCUs = 256;   // compute units of the target
 
+// the streaming kernel serves up to kLsRows positions when a block is a whole
+// number of 16-byte loads per thread and each wave's share of the hidden
+// dimension fits its registers
+static bool lm_stream_ok(long long n, int d) {
+  return n <= kLsRows && d % 512 == 0 && d <= kLsMaxD;
+}
+
+// the streaming kernel for d = 512 DM
+typedef void (*LmStreamFn)(const uint16_t*, const uint16_t*, const uint8_t*, const int32_t*,
+                           const int32_t*, int, int, int, int32_t*, int32_t*, RowOut, WavePartial*,
+                           int);
+static const LmStreamFn kLmStream[kLsMaxD / 512] = {
+    k_lm_stream<1>, k_lm_stream<2>, k_lm_stream<3>, k_lm_stream<4>,
+    k_lm_stream<5>, k_lm_stream<6>, k_lm_stream<7>, k_lm_stream<8>};
+
 struct LmPlan {
+  int small;     // 1: k_lm_stream; 0: the tiled kernel
   int m_tiles, n_tiles, n_split, tiles_per_split;
   size_t off_rows, off_partials, off_out, bytes;
 };
 
 // Row tiles cover the upper bound B*L (tiles past the device-side count exit
 // at once); the vocabulary is split so that about 512 workgroups run.
-static LmPlan lm_plan(int B, int L, int V, bool need_out) {
+static LmPlan lm_plan(int B, int L, int d, int V, bool need_out) {
   LmPlan p{};
   const long long n = (long long)B * L;
+  if (lm_stream_ok(n, d)) {
+    // one workgroup per compute unit, each a contiguous range of row blocks
+    p.small = 1;
+    const int nblk = (V + kLsBlk - 1) / kLsBlk;
+    p.n_split = nblk < kLmCUs ? nblk : kLmCUs;
+    p.off_rows = 256;
+    p.off_partials = p.off_rows + align256((size_t)n * 4);
+    p.off_out = p.off_partials + align256((size_t)n * p.n_split * sizeof(WavePartial));
+    p.bytes = p.off_out + (need_out ? 3 * align256((size_t)n * 4) : 0);
+    return p;
+  }
   p.m_tiles = (int)((n + kLmRows - 1) / kLmRows);
   p.n_tiles = (V + kLmCols - 1) / kLmCols;
   // one workgroup per CU at a time: pick the split with the shortest makespan
@@ -474,8 +703,9 @@ static bool lm_sizes_ok(int B, int L, int d, int V) {
   return (long long)B * L * d * 2 <= 0xffffffffLL && (long long)V * (d / 8) < 0x7fffffffLL;
 }
 
-// The partial kernel's dynamic LDS (128 KiB) is above the default limit; the
-// limit is raised once per device, before the first launch there.
+// The partial kernels' dynamic LDS (128 and up to 144 KiB) is above the
+// default limit; the limit is raised once per device, before the first launch
+// there.
 constexpr int kLmMaxDevices = 64;
 static std::atomic<bool> lm_lds_allowed[kLmMaxDevices];
 
@@ -485,9 +715,11 @@ static hipError_t lm_allow_lds() {
   if (e != hipSuccess) return e;
   if (dev >= 0 && dev < kLmMaxDevices && lm_lds_allowed[dev].load(std::memory_order_acquire))
     return hipSuccess;
-  const hipError_t a = hipFuncSetAttribute((const void*)k_lm_partial,
-                                           hipFuncAttributeMaxDynamicSharedMemorySize,
-                                           (int)kLmLdsBytes);
+  hipError_t a = hipFuncSetAttribute((const void*)k_lm_partial,
+                                     hipFuncAttributeMaxDynamicSharedMemorySize, (int)kLmLdsBytes);
+  for (int i = 0; i < kLsMaxD / 512 && a == hipSuccess; ++i)
+    a = hipFuncSetAttribute((const void*)kLmStream[i], hipFuncAttributeMaxDynamicSharedMemorySize,
+                            (int)kLsLdsBytes(512 * (i + 1)));
   if (a == hipSuccess && dev >= 0 && dev < kLmMaxDevices)
     lm_lds_allowed[dev].store(true, std::memory_order_release);
   return a;
@@ -501,12 +733,20 @@ static hipError_t lm_launch(const void* hidden, const void* weight, int B, int L
   WavePartial* part = (WavePartial*)(ws + p.off_partials);
   const hipError_t attr = lm_allow_lds();
   if (attr != hipSuccess) return attr;
-  hipLaunchKernelGGL(k_lm_zero, dim3(1), dim3(64), 0, st, count);
-  hipLaunchKernelGGL(k_lm_compact, dim3((unsigned)((B + 3) / 4)), dim3(256), 0, st, mask, bs, be, B,
-                     L, rows, count, out);
-  hipLaunchKernelGGL(k_lm_partial, dim3((unsigned)p.m_tiles, (unsigned)p.n_split), dim3(kLmThreads),
-                     kLmLdsBytes, st, (const uint16_t*)hidden, (const uint16_t*)weight, rows, count,
-                     d, V, p.tiles_per_split, (uint32_t)((size_t)B * L * d * 2), part, p.n_split);
+  if (p.small) {
+    // the streaming kernel compacts the candidates itself
+    hipLaunchKernelGGL(kLmStream[d / 512 - 1], dim3((unsigned)p.n_split), dim3(kLsWaves * kWave),
+                       kLsLdsBytes(d), st, (const uint16_t*)hidden, (const uint16_t*)weight, mask,
+                       bs, be, B, L, V, rows, count, out, part, p.n_split);
+  } else {
+    hipLaunchKernelGGL(k_lm_zero, dim3(1), dim3(64), 0, st, count);
+    hipLaunchKernelGGL(k_lm_compact, dim3((unsigned)((B + 3) / 4)), dim3(256), 0, st, mask, bs, be,
+                       B, L, rows, count, out);
+    hipLaunchKernelGGL(k_lm_partial, dim3((unsigned)p.m_tiles, (unsigned)p.n_split),
+                       dim3(kLmThreads), kLmLdsBytes, st, (const uint16_t*)hidden,
+                       (const uint16_t*)weight, rows, count, d, V, p.tiles_per_split,
+                       (uint32_t)((size_t)B * L * d * 2), part, p.n_split);
+  }
   const long long n = (long long)B * L;
   hipLaunchKernelGGL(k_lm_finish, dim3((unsigned)((n + 3) / 4)), dim3(256), 0, st, rows, count,
                      part, p.n_split, out);
@@ -523,7 +763,7 @@ fdllm_status fdllm_lmhead_workspace_size(int B, int L, int d, int V, size_t* byt
   if (!bytes) return FDLLM_ERR_INVALID_ARG;
   if (B < 0 || L < 1) return FDLLM_ERR_INVALID_ARG;
   if (!lm_sizes_ok(B, L, d, V)) return FDLLM_ERR_SIZE;
-  *bytes = lm_plan(B, L, V, true).bytes;
+  *bytes = lm_plan(B, L, d, V, true).bytes;
   return FDLLM_OK;
 }
 
@@ -535,7 +775,7 @@ static fdllm_status lm_common(const void* hidden, const void* weight, int B, int
   if (!hidden || !weight || !mask || !bs || !be) return FDLLM_ERR_INVALID_ARG;
   if (((uintptr_t)hidden % 16) != 0 || ((uintptr_t)weight % 16) != 0) return FDLLM_ERR_INVALID_ARG;
   const bool need_out = !out.tokens || !out.conf || !out.eps;
-  const LmPlan p = lm_plan(B, L, V, need_out);
+  const LmPlan p = lm_plan(B, L, d, V, need_out);
   if (!workspace || workspace_bytes < p.bytes) return FDLLM_ERR_WORKSPACE;
   char* ws = (char*)workspace;
   const size_t n = (size_t)B * L;

@@ -30,6 +30,17 @@ CASES = [
     (3, 100, 128, 777, "exact", 100),        # blocks beyond one wavefront
     (4, 32, 512, 2000, "random", 32),
     (2, 24, 4096, 8192, "random", 24),
+    # at most 32 positions and d a multiple of 512 up to 4096: the streaming kernel
+    (1, 32, 4096, 1001, "exact", 32),        # one sequence, partial last row block
+    (1, 13, 2048, 3000, "random", 13),
+    (1, 5, 4096, 10, "exact", 5),            # two row blocks, one per workgroup
+    (1, 32, 1024, 1001, "exact", 32),
+    (1, 20, 512, 3001, "random", 20),
+    (1, 32, 1536, 2000, "exact", 32),
+    (4, 8, 1024, 2500, "exact", 5),          # several sequences, windows inside them
+    (1, 32, 64, 1000, "exact", 32),          # d not a multiple of 512: the tiled kernel
+    (2, 30, 192, 777, "exact", 30),          # 33..64 positions
+    (1, 7, 128, 5000, "random", 7),
 ]
 
 
@@ -152,6 +163,24 @@ def test_lmhead_decode_step_eta_tensor(gpu):
     assert np.array_equal(xx.cpu().numpy()[ok], r.x[ok])
     assert np.array_equal(mk.cpu().numpy()[ok], r.mask[ok])
     say(f"  commits {int(n.clamp(min=0).sum())}, flagged {nf} (matching {nfm})")
+
+
+@pytest.mark.parametrize("d", [512, 4096, 192])
+def test_lmhead_no_candidates(gpu, d):
+    """No masked position inside any window: every output is the default."""
+    B, L, V = 2, 16, 700
+    g = torch.Generator().manual_seed(d)
+    hidden = torch.randn((B, L, d), generator=g).to(torch.bfloat16).cuda()
+    weight = torch.randn((V, d), generator=g).to(torch.bfloat16).cuda()
+    mask = torch.zeros((B, L), dtype=torch.uint8)
+    mask[1, 10:] = 1                                   # masked, but outside the window
+    start = torch.tensor([0, 2], dtype=torch.int32)
+    end = torch.tensor([16, 8], dtype=torch.int32)
+    say(f"[lmhead no candidates] d={d}")
+    out = _gpu_conf(gpu, hidden, weight, mask.cuda(), start.cuda(), end.cuda())
+    check_defaults(*[t.cpu().numpy() for t in out], mask.numpy(), start.numpy(), end.numpy(),
+                   range(B))
+    assert not candidates(mask.numpy(), start.numpy(), end.numpy(), range(B))
 
 
 def test_lmhead_rejects_bad_shapes(gpu):
