@@ -311,7 +311,7 @@ def per_workload_report(fd, torch, workloads, dev, stream_gbps, reps):
     d_model = 4096
     gw = torch.Generator(device=dev).manual_seed(2606)
     weight = (torch.randn((workloads.V_LLADA, d_model), generator=gw, device=dev) / 64).to(torch.bfloat16)
-    for B_lm in (8, 128):
+    for B_lm in (1, 8, 128):
         L_lm = 32
         hid = torch.randn((B_lm, L_lm, d_model), generator=gw, device=dev).to(torch.bfloat16)
         mk = torch.ones((B_lm, L_lm), dtype=torch.uint8, device=dev)
@@ -348,6 +348,7 @@ def per_workload_report(fd, torch, workloads, dev, stream_gbps, reps):
         rows.append({"workload": "lmhead", "shape": f"{B_lm * L_lm} positions, d={d_model}, V={workloads.V_LLADA}",
                      "fused_ms": 1e3 * med(tf), "fused_TFLOPs": flops / med(tf) / 1e12,
                      "frac_of_bf16_peak": flops / med(tf) / 2.5e15,
+                     "W_TBps": 2.0 * workloads.V_LLADA * d_model / med(tf) / 1e12,
                      "unfused_gemm_ms": 1e3 * med(tg), "unfused_pass_ms": 1e3 * med(tp),
                      "unfused_TFLOPs": flops / (med(tg) + med(tp)) / 1e12,
                      "logits_bytes_avoided": B_lm * L_lm * workloads.V_LLADA * 2})
@@ -403,12 +404,14 @@ def per_workload_markdown(rows, stress, stream_gbps, cmd) -> str:
         out += ["", "LM head fused with the vocabulary pass (`fdllm_lmhead_confidence`: bf16 hidden "
                 "states x bf16 output embedding on the matrix cores, online softmax in the epilogue, no "
                 "logits stored) against the unfused pair (hipBLASLt GEMM to bf16 logits via torch.matmul, "
-                "then `fdllm_confidence`); HIP-event medians, each event pair around 4 back-to-back calls:", "",
-                "| shape | fused ms | fused TFLOP/s | % of 2.5 PFLOP/s | GEMM ms | pass ms | unfused TFLOP/s | logits not stored |",
-                "|---|---|---|---|---|---|---|---|"]
+                "then `fdllm_confidence`); HIP-event medians, each event pair around 4 back-to-back calls.  "
+                "32 positions run the streaming kernel (bound by the read of W, 2 V d bytes), larger "
+                "shapes the tiled MFMA kernel:", "",
+                "| shape | fused ms | fused TFLOP/s | % of 2.5 PFLOP/s | W read TB/s | GEMM ms | pass ms | unfused TFLOP/s | logits not stored |",
+                "|---|---|---|---|---|---|---|---|---|"]
         for r in lm:
             out.append(f"| {r['shape']} | {r['fused_ms']:.3f} | {r['fused_TFLOPs']:.0f} | "
-                       f"{100 * r['frac_of_bf16_peak']:.1f} | {r['unfused_gemm_ms']:.3f} | "
+                       f"{100 * r['frac_of_bf16_peak']:.1f} | {r['W_TBps']:.2f} | {r['unfused_gemm_ms']:.3f} | "
                        f"{r['unfused_pass_ms']:.3f} | {r['unfused_TFLOPs']:.0f} | "
                        f"{r['logits_bytes_avoided'] / 1e6:.0f} MB |")
     return "\n".join(out) + "\n"
