@@ -428,10 +428,10 @@ constexpr int kLsRows = 32;        // positions served (two 16-column MFMA block
 constexpr int kLsWaves = 8;
 constexpr int kLsBlk = 8;          // vocabulary rows per block
 constexpr int kLsMaxD = 4096;      // hidden operands held in registers: d / 8 per wave
-// two row blocks and the waves' partial products (144 KiB at d = 4096)
-constexpr size_t kLsLdsBytes(int d) {
-  return 2 * (size_t)kLsBlk * d * 2 + (size_t)kLsWaves * 2 * kWave * sizeof(f32x4);
-}
+constexpr size_t kLsRedBytes = (size_t)kLsWaves * 2 * kWave * sizeof(f32x4);  // 16 KiB
+// two row blocks and two sets of the waves' partial products (160 KiB at
+// d = 4096, all of a CU's LDS)
+constexpr size_t kLsLdsBytes(int d) { return 2 * (size_t)kLsBlk * d * 2 + 2 * kLsRedBytes; }
 
 __device__ __forceinline__ int ls_swz(int r) { return r & 7; }
 
@@ -449,8 +449,10 @@ k_lm_stream(const uint16_t* __restrict__ hidden, const uint16_t* __restrict__ we
   constexpr int vec_row = d / 8;                             // 16-byte vectors per row
   constexpr uint32_t blk_bytes = (uint32_t)kLsBlk * d * 2;
   extern __shared__ __attribute__((aligned(1024))) char ls_lds[];
-  __shared__ int32_t cand_rows[kLsRows];
-  __shared__ int cand_n;
+  // the candidate list sits in the second set of partial products, first
+  // written after the loop's second barrier
+  int32_t* cand_rows = reinterpret_cast<int32_t*>(ls_lds + 2 * blk_bytes + kLsRedBytes);
+  int* cand_n = reinterpret_cast<int*>(cand_rows + kLsRows);
   const int t = threadIdx.x;
   const int lane = t % kWave;
   const int wave = __builtin_amdgcn_readfirstlane(t / kWave);
@@ -469,7 +471,7 @@ k_lm_stream(const uint16_t* __restrict__ hidden, const uint16_t* __restrict__ we
     const unsigned long long bal = __ballot(cand);
     const int idx = __popcll(bal & ((1ull << lane) - 1ull));
     if (cand) cand_rows[idx] = lane;
-    if (lane == 0) cand_n = __popcll(bal);
+    if (lane == 0) *cand_n = __popcll(bal);
     if (g == 0) {
       if (cand) rows[idx] = lane;
       else if (lane < n) store_default(out, lane);
@@ -477,13 +479,14 @@ k_lm_stream(const uint16_t* __restrict__ hidden, const uint16_t* __restrict__ we
     }
   }
   __syncthreads();
-  const int nrows = cand_n;
+  const int nrows = *cand_n;
   if (nrows == 0) return;
 
   const int nblk = (V + kLsBlk - 1) / kLsBlk;
   const int b_beg = (int)((long long)g * nblk / G), b_end = (int)((long long)(g + 1) * nblk / G);
   const int cnt = b_end - b_beg;
-  float* red = reinterpret_cast<float*>(ls_lds + 2 * blk_bytes);  // f32x4 [wave][ni][lane]
+  // partial products of block i in set i % 2: f32x4 [wave][ni][lane]
+  float* red = reinterpret_cast<float*>(ls_lds + 2 * blk_bytes);
   const int k0 = wave * (d / kLsWaves);
 
   // the hidden operands of this wave's share, for positions 16 ni + l % 16
@@ -532,6 +535,24 @@ k_lm_stream(const uint16_t* __restrict__ hidden, const uint16_t* __restrict__ we
   // ni = fp / 16, lane 16 (fr / 4) + fp % 16, element fr % 4
   const int red_idx = ((fp / 16) * kWave + 16 * (fr / 4) + fp % 16) * 4 + fr % 4;
   LmState st{kNegInf, kRefFloor, 0.0, 0x7fffffff};
+  // sums block i's 8 partial products of (fr, fp) and folds the logit
+  auto fold = [&](int i) {
+    const float* rs = red + (i & 1) * (kLsRedBytes / sizeof(float));
+    const int v = (b_beg + i) * kLsBlk + fr;
+    if (folds && v < V) {
+      float x = rs[red_idx];
+#pragma unroll
+      for (int w = 1; w < kLsWaves; ++w) x += rs[w * 2 * kWave * 4 + red_idx];
+      if (x > st.M) {
+        const float Kn = exp_ref(x);
+        st.S = rescale(st.S, st.K, Kn);
+        st.K = Kn;
+        st.M = x;
+        st.first = v;
+      }
+      st.S += (double)term(x, st.K);
+    }
+  };
   // operand address of this lane in a buffer: row l % 8 (rows 8..15 of the
   // MFMA block repeat rows 0..7), vector k0 / 8 + 4 c + l / 16
   const int ar = lane % kLsBlk;
@@ -546,49 +567,41 @@ k_lm_stream(const uint16_t* __restrict__ hidden, const uint16_t* __restrict__ we
   if (cnt > 1) load_regs(1);
   for (int it = 0; it < cnt; ++it) {
     const int buf = it & 1;
-    // the block is in LDS, and every thread has folded the previous block's
-    // logits (the partial products may be overwritten)
+    // one barrier per block: block it is in LDS (stored during the previous
+    // iteration), the previous block's partial products are complete, and
+    // the fold that read this iteration's set (two blocks back) is done
     __syncthreads();
     const u32x4* bl = reinterpret_cast<const u32x4*>(ls_lds + buf * blk_bytes);
-    f32x4 acc[2];
+    // two accumulators per column block halve the dependent MFMA chain
+    f32x4 acc[2][2];
 #pragma unroll
-    for (int ni = 0; ni < 2; ++ni)
+    for (int h = 0; h < 2; ++h)
 #pragma unroll
-      for (int i = 0; i < 4; ++i) acc[ni][i] = 0.0f;
+      for (int ni = 0; ni < 2; ++ni)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) acc[h][ni][i] = 0.0f;
 #pragma unroll
     for (int c = 0; c < NC; ++c) {
       const int sv = k0 / 8 + 4 * c + lane / 16;
       const bf16x8 a = __builtin_bit_cast(bf16x8, bl[a_row + (sv ^ ls_swz(ar))]);
 #pragma unroll
       for (int ni = 0; ni < 2; ++ni)
-        acc[ni] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, __builtin_bit_cast(bf16x8, hb[c][ni]),
-                                                          acc[ni], 0, 0, 0);
+        acc[c & 1][ni] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+            a, __builtin_bit_cast(bf16x8, hb[c][ni]), acc[c & 1][ni], 0, 0, 0);
     }
-    f32x4* redv = reinterpret_cast<f32x4*>(red);
+    f32x4* redv = reinterpret_cast<f32x4*>(red + buf * (kLsRedBytes / sizeof(float)));
 #pragma unroll
-    for (int ni = 0; ni < 2; ++ni) redv[(wave * 2 + ni) * kWave + lane] = acc[ni];
-    __syncthreads();
-    const int v = (b_beg + it) * kLsBlk + fr;
-    if (folds && v < V) {
-      float x = red[red_idx];
-#pragma unroll
-      for (int w = 1; w < kLsWaves; ++w) x += red[w * 2 * kWave * 4 + red_idx];
-      if (x > st.M) {
-        const float Kn = exp_ref(x);
-        st.S = rescale(st.S, st.K, Kn);
-        st.K = Kn;
-        st.M = x;
-        st.first = v;
-      }
-      st.S += (double)term(x, st.K);
-    }
+    for (int ni = 0; ni < 2; ++ni) redv[(wave * 2 + ni) * kWave + lane] = acc[0][ni] + acc[1][ni];
+    // the previous block's logits, while other waves still multiply
+    if (it > 0) fold(it - 1);
     // the next block into the buffer every wave finished reading before the
     // barrier above, then the block after it into the registers
     if (it + 1 < cnt) store_lds(buf ^ 1);
     if (it + 2 < cnt) load_regs(it + 2);
   }
-  // the row states of a position meet in LDS once every wave is done with
-  // the blocks
+  __syncthreads();
+  fold(cnt - 1);
+  // the row states of a position meet in LDS (the row buffers are free)
   __syncthreads();
   WavePartial* xs = reinterpret_cast<WavePartial*>(ls_lds);
   if (folds) xs[fr * kLsRows + fp] = WavePartial{st.M, st.K, st.S, st.first};
