@@ -617,6 +617,250 @@ k_lm_stream(const uint16_t* __restrict__ hidden, const uint16_t* __restrict__ we
   }
 }
 
+// ---------------------------------------------------------------------------
+// 33..64 positions: the hidden dimension split over workgroups
+// ---------------------------------------------------------------------------
+// A CU's registers hold the hidden operands of about 32 positions at d = 4096,
+// so for up to 32 S positions the hidden dimension is cut into S parts of
+// d / S elements and workgroup g takes part g % S of the contiguous row range
+// of group g / S: W is still read once, in blocks of 8 S rows x d / S
+// elements (16 d bytes, 64 KiB at d = 4096; each row piece contiguous).  Wave
+// w owns the 16 positions of column block w % 2S and the (w / 2S)-th of the
+// part's elements (4 / S waves per column block), with those hidden operands
+// in registers (128 VGPRs at d = 4096).  The waves' products of a block meet
+// in LDS, where the next iteration adds the halves and writes the block's
+// logits over the part (float32, MFMA accumulation) as one contiguous run of
+// 16-byte vectors: plogits[part][v][position].  k_lm_ksum adds the S parts in
+// order and folds them.  The plan uses S = 2: with S = 4 (128 positions) the
+// partial logits' extra traffic (2 x 259 MB at V = 126464) and the 8-fold
+// LDS operand reads left it no faster than the tiled kernel.
+constexpr int kKsWaves = 8;
+
+// two sets of the waves' products: 8 waves x S / 2 row blocks x 1 KiB each
+template <int S>
+constexpr size_t ks_red_bytes() {
+  return 2 * (size_t)kKsWaves * (S / 2) * kWave * sizeof(f32x4);
+}
+// two row blocks and the products (144 KiB for S = 2 at d = 4096)
+template <int S>
+constexpr size_t ks_lds_bytes(int d) {
+  return 2 * (size_t)16 * d + ks_red_bytes<S>();
+}
+
+template <int DM, int S>
+__global__ void __launch_bounds__(kKsWaves * kWave)
+k_lm_kstream(const uint16_t* __restrict__ hidden, const uint16_t* __restrict__ weight,
+             const uint8_t* __restrict__ mask, const int32_t* __restrict__ bstart,
+             const int32_t* __restrict__ bend, int B, int L, int V, int32_t* __restrict__ rows,
+             int32_t* __restrict__ count, RowOut out, float* __restrict__ plogits) {
+  constexpr int d = DM * 512;
+  constexpr int dk = d / S;                                 // elements per part
+  constexpr int NP = kLsRows * S;                           // positions served
+  constexpr int NB = NP / 16;                               // 16-column MFMA blocks
+  constexpr int KW = kKsWaves / NB;                         // waves per column block
+  constexpr int dw = dk / KW;                               // elements per wave (d / 4)
+  constexpr int NC = dw / 32;                               // 32-element chunks per wave
+  constexpr int R = 8 * S;                                  // rows per block
+  constexpr int MB = R / 16;                                // 16-row MFMA blocks per block
+  constexpr int vec_part = dk / 8;                          // 16-byte vectors per row piece
+  constexpr int vec_row = d / 8;
+  constexpr uint32_t blk_bytes = (uint32_t)R * dk * 2;
+  constexpr int NL = (int)(blk_bytes / (kKsWaves * kWave * 16));  // loads per thread and block
+  static_assert(KW * NB == kKsWaves && MB >= 1 && NL == DM && NC >= 1, "k-split shape");
+  extern __shared__ __attribute__((aligned(1024))) char ks_lds[];
+  // products: float [set][wave][row block][element][lane]
+  float* red = reinterpret_cast<float*>(ks_lds + 2 * blk_bytes);
+  constexpr int red_set = kKsWaves * MB * 4 * kWave;              // floats per set
+  // the candidate list sits in the second set, first written after the
+  // loop's second barrier
+  int32_t* cand_rows = reinterpret_cast<int32_t*>(red + red_set);
+  int* cand_n = cand_rows + NP;
+  const int t = threadIdx.x;
+  const int lane = t % kWave;
+  const int wave = __builtin_amdgcn_readfirstlane(t / kWave);
+  const int g = blockIdx.x;
+  const int kp = g % S;                                     // part of the hidden dimension
+  const int gr = g / S, GR = gridDim.x / S;                 // row-range group
+
+  // the candidate positions, in position order (B L <= NP)
+  if (wave == 0) {
+    const int n = B * L;
+    int base = 0;
+    for (int q0 = 0; q0 < NP; q0 += kWave) {
+      const int q = q0 + lane;
+      bool cand = false;
+      if (q < n) {
+        const int b = q / L, i = q % L;
+        const int s = bstart[b], e = bend[b];
+        cand = window_ok(s, e, L) && i >= s && i < e && mask[q] != 0;
+      }
+      const unsigned long long bal = __ballot(cand);
+      const int idx = base + __popcll(bal & ((1ull << lane) - 1ull));
+      if (cand) cand_rows[idx] = q;
+      if (g == 0) {
+        if (cand) rows[idx] = q;
+        else if (q < n) store_default(out, q);
+      }
+      base += __popcll(bal);
+    }
+    if (lane == 0) {
+      *cand_n = base;
+      if (g == 0) *count = base;
+    }
+  }
+  __syncthreads();
+  const int nrows = *cand_n;
+  if (nrows == 0) return;
+
+  const int nblk = (V + R - 1) / R;
+  const int b_beg = (int)((long long)gr * nblk / GR), b_end = (int)((long long)(gr + 1) * nblk / GR);
+  const int cnt = b_end - b_beg;
+  const int cb = wave % NB, kw = wave / NB;
+  const int k0 = kp * dk + kw * dw;                         // this wave's first element
+
+  // hidden operands of positions 16 cb + l % 16 (past the count: the first
+  // row; their logits are written but never folded)
+  u32x4 hb[NC];
+  {
+    const int q = 16 * cb + lane % 16;
+    const uint16_t* h = hidden + (size_t)cand_rows[q < nrows ? q : 0] * d + k0 + 8 * (lane / 16);
+#pragma unroll
+    for (int c = 0; c < NC; ++c) hb[c] = *reinterpret_cast<const u32x4*>(h + 32 * c);
+  }
+  // block loads as in k_lm_stream, over the part's row pieces; LDS slot
+  // (row r, vector s) holds the piece's vector s ^ (r % 16), so the 16 rows
+  // an operand read touches sit in distinct banks
+  const u32x4* wv = reinterpret_cast<const u32x4*>(weight);
+  u32x4 stg[NL];
+  auto load_regs = [&](int i) {
+    const int vb = (b_beg + i) * R;
+#pragma unroll
+    for (int j = 0; j < NL; ++j) {
+      const int slot = j * kKsWaves * kWave + t;
+      const int v = min(vb + slot / vec_part, V - 1);       // rows past V repeat the last
+      stg[j] = __builtin_nontemporal_load(wv + (size_t)v * vec_row + kp * vec_part + slot % vec_part);
+    }
+  };
+  auto store_lds = [&](int buf) {
+    u32x4* bl = reinterpret_cast<u32x4*>(ks_lds + buf * blk_bytes);
+#pragma unroll
+    for (int j = 0; j < NL; ++j) {
+      const int slot = j * kKsWaves * kWave + t;
+      const int r = slot / vec_part, sv = slot % vec_part;
+      bl[r * vec_part + (sv ^ (r & 15))] = stg[j];
+    }
+  };
+  // logits of block i from the products in set i % 2: the block's R x NP
+  // floats are contiguous in plogits, one 16-byte vector (4 positions of a
+  // row) per thread and step; in the products, row r, position p of column
+  // block cb sits at element r % 4 of lanes 16 ((r % 16) / 4) + p % 16 of the
+  // waves kw NB + cb, row block r / 16
+  auto store_logits = [&](int i) {
+    constexpr int NV = R * NP / 4;                          // vectors per block
+    const float* rs = red + (i & 1) * red_set;
+    const int v0 = (b_beg + i) * R;
+#pragma unroll
+    for (int j = 0; j < (NV + kKsWaves * kWave - 1) / (kKsWaves * kWave); ++j) {
+      const int x = j * kKsWaves * kWave + t;
+      const int r = x / (NP / 4), p = 4 * (x % (NP / 4));
+      if (x < NV && v0 + r < V) {
+        const int cbx = p / 16;
+        const int off = ((r / 16) * 4 + r % 4) * kWave + 16 * ((r % 16) / 4) + p % 16;
+        f32x4 sum = *reinterpret_cast<const f32x4*>(rs + cbx * MB * 4 * kWave + off);
+#pragma unroll
+        for (int k = 1; k < KW; ++k)
+          sum += *reinterpret_cast<const f32x4*>(rs + (k * NB + cbx) * MB * 4 * kWave + off);
+        *reinterpret_cast<f32x4*>(plogits + ((size_t)kp * V + v0 + r) * NP + p) = sum;
+      }
+    }
+  };
+  const int ar = lane % 16;                                 // operand row within an MFMA block
+
+  load_regs(0);
+  store_lds(0);
+  __builtin_amdgcn_s_waitcnt(0x0f70);                       // vmcnt(0), as in k_lm_stream
+  if (cnt > 1) load_regs(1);
+  for (int it = 0; it < cnt; ++it) {
+    const int buf = it & 1;
+    // block it is in LDS; the products of block it - 1 are complete, and
+    // those of block it - 2 (this iteration's set) have been written out
+    __syncthreads();
+    if (it > 0) store_logits(it - 1);
+    const u32x4* bl = reinterpret_cast<const u32x4*>(ks_lds + buf * blk_bytes);
+    f32x4 acc[2][MB];
+#pragma unroll
+    for (int h = 0; h < 2; ++h)
+#pragma unroll
+      for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+        for (int e = 0; e < 4; ++e) acc[h][mb][e] = 0.0f;
+#pragma unroll
+    for (int c = 0; c < NC; ++c) {
+      const int sv = kw * (dw / 8) + 4 * c + lane / 16;
+#pragma unroll
+      for (int mb = 0; mb < MB; ++mb) {
+        const bf16x8 a = __builtin_bit_cast(bf16x8, bl[(16 * mb + ar) * vec_part + (sv ^ ar)]);
+        acc[c & 1][mb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, __builtin_bit_cast(bf16x8, hb[c]),
+                                                                 acc[c & 1][mb], 0, 0, 0);
+      }
+    }
+    float* ws_ = red + (it & 1) * red_set + wave * MB * 4 * kWave + lane;
+#pragma unroll
+    for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) ws_[(mb * 4 + e) * kWave] = acc[0][mb][e] + acc[1][mb][e];
+    if (it + 1 < cnt) store_lds(buf ^ 1);
+    if (it + 2 < cnt) load_regs(it + 2);
+  }
+  __syncthreads();
+  store_logits(cnt - 1);
+}
+
+// Adds the S parts' logits of every candidate position, in part order, and
+// folds them: workgroup j takes the vocabulary entries [j chunk, (j+1) chunk);
+// thread t takes the 4 positions 4 (t % Q) .. +3 (Q = NP / 4) at every
+// (256 / Q)-th entry; the threads of a position are combined in order at the
+// end, one partial per (position, workgroup) for k_lm_finish.
+template <int S>
+__global__ void __launch_bounds__(256)
+k_lm_ksum(const float* __restrict__ plogits, const int32_t* __restrict__ count, int V, int chunk,
+          WavePartial* __restrict__ partials, int n_split) {
+  constexpr int NP = kLsRows * S, Q = NP / 4, VS = 256 / Q;
+  __shared__ WavePartial xs[VS][NP];
+  const int t = threadIdx.x, q = t % Q, vs = t / Q;
+  const int n = *count;
+  if (n == 0) return;
+  const int v0 = blockIdx.x * chunk, v1 = min(V, v0 + chunk);
+  LmState st[4];
+#pragma unroll
+  for (int e = 0; e < 4; ++e) st[e] = LmState{kNegInf, kRefFloor, 0.0, 0x7fffffff};
+  for (int v = v0 + vs; v < v1; v += VS) {
+    f32x4 x = *reinterpret_cast<const f32x4*>(plogits + (size_t)v * NP + 4 * q);
+#pragma unroll
+    for (int k = 1; k < S; ++k) x += *reinterpret_cast<const f32x4*>(plogits + ((size_t)k * V + v) * NP + 4 * q);
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      if (x[e] > st[e].M) {
+        const float Kn = exp_ref(x[e]);
+        st[e].S = rescale(st[e].S, st[e].K, Kn);
+        st[e].K = Kn;
+        st[e].M = x[e];
+        st[e].first = v;
+      }
+      st[e].S += (double)term(x[e], st[e].K);
+    }
+  }
+#pragma unroll
+  for (int e = 0; e < 4; ++e) xs[vs][4 * q + e] = WavePartial{st[e].M, st[e].K, st[e].S, st[e].first};
+  __syncthreads();
+  if (t < n) {
+    LmState c = {xs[0][t].m, xs[0][t].K, xs[0][t].S, xs[0][t].first};
+#pragma unroll
+    for (int r = 1; r < VS; ++r) lm_combine(c, xs[r][t].m, xs[r][t].K, xs[r][t].S, xs[r][t].first);
+    partials[(size_t)t * n_split + blockIdx.x] = WavePartial{c.M, c.K, c.S, c.first};
+  }
+}
+
 // Per candidate row, one wavefront: lane l combines the splits l, l+64, ...
 // of the row's contiguous partials, then a fixed butterfly over the lanes
 // (both partners of every step form the same sum) and the finish.
@@ -649,11 +893,15 @@ k_lm_finish(const int32_t* __restrict__ rows, const int32_t* __restrict__ count,
 // ---------------------------------------------------------------------------
 constexpr int kLmCUs = 256;   // compute units of the target
 
-// the streaming kernel serves up to kLsRows positions when a block is a whole
-// number of 16-byte loads per thread and each wave's share of the hidden
-// dimension fits its registers
-static bool lm_stream_ok(long long n, int d) {
-  return n <= kLsRows && d % 512 == 0 && d <= kLsMaxD;
+// Parts of the hidden dimension for the streaming kernels: 1 (k_lm_stream)
+// up to kLsRows positions, 2 (k_lm_kstream) up to 2 kLsRows, when
+// a block is a whole number of 16-byte loads per thread and each wave's share
+// of the hidden operands fits its registers; 0: the tiled kernel.
+static int lm_kparts(long long n, int d) {
+  if (d > kLsMaxD) return 0;
+  if (n <= kLsRows) return d % 512 == 0 ? 1 : 0;
+  if (n <= 2 * kLsRows) return d % 1024 == 0 ? 2 : 0;
+  return 0;
 }
 
 // the streaming kernel for d = 512 DM
@@ -664,8 +912,18 @@ static const LmStreamFn kLmStream[kLsMaxD / 512] = {
     k_lm_stream<1>, k_lm_stream<2>, k_lm_stream<3>, k_lm_stream<4>,
     k_lm_stream<5>, k_lm_stream<6>, k_lm_stream<7>, k_lm_stream<8>};
 
+// the k-split kernel (S = 2) for d = 1024 i
+typedef void (*LmKStreamFn)(const uint16_t*, const uint16_t*, const uint8_t*, const int32_t*,
+                            const int32_t*, int, int, int, int32_t*, int32_t*, RowOut, float*);
+static const LmKStreamFn kLmKStream2[kLsMaxD / 1024] = {
+    k_lm_kstream<2, 2>, k_lm_kstream<4, 2>, k_lm_kstream<6, 2>, k_lm_kstream<8, 2>};
+constexpr int kKsSplits = 512;     // k_lm_ksum workgroups (vocabulary chunks)
+
 struct LmPlan {
-  int small;     // 1: k_lm_stream; 0: the tiled kernel
+  int small;     // parts of the hidden dimension: 1 k_lm_stream, 2 k_lm_kstream; 0 tiled
+  int groups;    // k_lm_kstream: row-range groups (S groups workgroups)
+  int chunk;     // k_lm_ksum: vocabulary entries per workgroup
+  size_t off_plogits;
   int m_tiles, n_tiles, n_split, tiles_per_split;
   size_t off_rows, off_partials, off_out, bytes;
 };
@@ -675,7 +933,8 @@ struct LmPlan {
 static LmPlan lm_plan(int B, int L, int d, int V, bool need_out) {
   LmPlan p{};
   const long long n = (long long)B * L;
-  if (lm_stream_ok(n, d)) {
+  const int S = lm_kparts(n, d);
+  if (S == 1) {
     // one workgroup per compute unit, each a contiguous range of row blocks
     p.small = 1;
     const int nblk = (V + kLsBlk - 1) / kLsBlk;
@@ -683,6 +942,21 @@ static LmPlan lm_plan(int B, int L, int d, int V, bool need_out) {
     p.off_rows = 256;
     p.off_partials = p.off_rows + align256((size_t)n * 4);
     p.off_out = p.off_partials + align256((size_t)n * p.n_split * sizeof(WavePartial));
+    p.bytes = p.off_out + (need_out ? 3 * align256((size_t)n * 4) : 0);
+    return p;
+  }
+  if (S > 1) {
+    // S workgroups (one per part) per row range, one workgroup per compute
+    // unit; the parts' logits of all 32 S positions in the workspace
+    p.small = S;
+    const int nblk = (V + 8 * S - 1) / (8 * S);
+    p.groups = nblk < kLmCUs / S ? nblk : kLmCUs / S;
+    p.chunk = (V + kKsSplits - 1) / kKsSplits;
+    p.n_split = (V + p.chunk - 1) / p.chunk;
+    p.off_rows = 256;
+    p.off_partials = p.off_rows + align256((size_t)n * 4);
+    p.off_plogits = p.off_partials + align256((size_t)n * p.n_split * sizeof(WavePartial));
+    p.off_out = p.off_plogits + align256((size_t)S * V * kLsRows * S * sizeof(float));
     p.bytes = p.off_out + (need_out ? 3 * align256((size_t)n * 4) : 0);
     return p;
   }
@@ -733,6 +1007,9 @@ static hipError_t lm_allow_lds() {
   for (int i = 0; i < kLsMaxD / 512 && a == hipSuccess; ++i)
     a = hipFuncSetAttribute((const void*)kLmStream[i], hipFuncAttributeMaxDynamicSharedMemorySize,
                             (int)kLsLdsBytes(512 * (i + 1)));
+  for (int i = 0; i < kLsMaxD / 1024 && a == hipSuccess; ++i)
+    a = hipFuncSetAttribute((const void*)kLmKStream2[i], hipFuncAttributeMaxDynamicSharedMemorySize,
+                            (int)ks_lds_bytes<2>(1024 * (i + 1)));
   if (a == hipSuccess && dev >= 0 && dev < kLmMaxDevices)
     lm_lds_allowed[dev].store(true, std::memory_order_release);
   return a;
@@ -746,7 +1023,17 @@ static hipError_t lm_launch(const void* hidden, const void* weight, int B, int L
   WavePartial* part = (WavePartial*)(ws + p.off_partials);
   const hipError_t attr = lm_allow_lds();
   if (attr != hipSuccess) return attr;
-  if (p.small) {
+  if (p.small > 1) {
+    // the k-split kernel compacts the candidates itself
+    const uint16_t* h = (const uint16_t*)hidden;
+    const uint16_t* w = (const uint16_t*)weight;
+    float* plog = (float*)(ws + p.off_plogits);
+    const dim3 grid((unsigned)(p.groups * 2)), block(kKsWaves * kWave);
+    hipLaunchKernelGGL(kLmKStream2[d / 1024 - 1], grid, block, ks_lds_bytes<2>(d), st, h, w, mask, bs,
+                       be, B, L, V, rows, count, out, plog);
+    hipLaunchKernelGGL(k_lm_ksum<2>, dim3((unsigned)p.n_split), dim3(256), 0, st, plog, count, V,
+                       p.chunk, part, p.n_split);
+  } else if (p.small) {
     // the streaming kernel compacts the candidates itself
     hipLaunchKernelGGL(kLmStream[d / 512 - 1], dim3((unsigned)p.n_split), dim3(kLsWaves * kWave),
                        kLsLdsBytes(d), st, (const uint16_t*)hidden, (const uint16_t*)weight, mask,

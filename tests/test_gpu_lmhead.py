@@ -39,6 +39,15 @@ CASES = [
     (1, 32, 1536, 2000, "exact", 32),
     (4, 8, 1024, 2500, "exact", 5),          # several sequences, windows inside them
     (1, 32, 64, 1000, "exact", 32),          # d not a multiple of 512: the tiled kernel
+    # 33..64 positions, d a multiple of 1024: the k-split kernel
+    (2, 32, 4096, 126464, "exact", 32),      # two sequences' blocks at LLaDA's sizes
+    (1, 64, 1024, 3001, "random", 64),
+    (2, 20, 3072, 999, "exact", 20),
+    (1, 50, 4096, 700, "random", 50),        # fewer row blocks than workgroup groups
+    # more positions: the tiled kernel
+    (4, 32, 2048, 5000, "exact", 32),
+    (3, 40, 4096, 2000, "random", 40),
+    (1, 100, 2048, 777, "exact", 100),
     (2, 30, 192, 777, "exact", 30),          # 33..64 positions
     (1, 7, 128, 5000, "random", 7),
 ]
@@ -165,10 +174,10 @@ def test_lmhead_decode_step_eta_tensor(gpu):
     say(f"  commits {int(n.clamp(min=0).sum())}, flagged {nf} (matching {nfm})")
 
 
-@pytest.mark.parametrize("d", [512, 4096, 192])
-def test_lmhead_no_candidates(gpu, d):
+@pytest.mark.parametrize("L,d", [(16, 512), (16, 4096), (16, 192), (30, 4096), (50, 2048)])
+def test_lmhead_no_candidates(gpu, L, d):
     """No masked position inside any window: every output is the default."""
-    B, L, V = 2, 16, 700
+    B, V = 2, 700
     g = torch.Generator().manual_seed(d)
     hidden = torch.randn((B, L, d), generator=g).to(torch.bfloat16).cuda()
     weight = torch.randn((V, d), generator=g).to(torch.bfloat16).cuda()
@@ -176,7 +185,7 @@ def test_lmhead_no_candidates(gpu, d):
     mask[1, 10:] = 1                                   # masked, but outside the window
     start = torch.tensor([0, 2], dtype=torch.int32)
     end = torch.tensor([16, 8], dtype=torch.int32)
-    say(f"[lmhead no candidates] d={d}")
+    say(f"[lmhead no candidates] L={L} d={d}")
     out = _gpu_conf(gpu, hidden, weight, mask.cuda(), start.cuda(), end.cuda())
     check_defaults(*[t.cpu().numpy() for t in out], mask.numpy(), start.numpy(), end.numpy(),
                    range(B))
