@@ -311,7 +311,7 @@ def per_workload_report(fd, torch, workloads, dev, stream_gbps, reps):
     d_model = 4096
     gw = torch.Generator(device=dev).manual_seed(2606)
     weight = (torch.randn((workloads.V_LLADA, d_model), generator=gw, device=dev) / 64).to(torch.bfloat16)
-    for B_lm in (1, 8, 128):
+    for B_lm in (1, 2, 8, 128):
         L_lm = 32
         hid = torch.randn((B_lm, L_lm, d_model), generator=gw, device=dev).to(torch.bfloat16)
         mk = torch.ones((B_lm, L_lm), dtype=torch.uint8, device=dev)
@@ -405,8 +405,8 @@ def per_workload_markdown(rows, stress, stream_gbps, cmd) -> str:
                 "states x bf16 output embedding on the matrix cores, online softmax in the epilogue, no "
                 "logits stored) against the unfused pair (hipBLASLt GEMM to bf16 logits via torch.matmul, "
                 "then `fdllm_confidence`); HIP-event medians, each event pair around 4 back-to-back calls.  "
-                "32 positions run the streaming kernel (bound by the read of W, 2 V d bytes), larger "
-                "shapes the tiled MFMA kernel:", "",
+                "32 positions run the streaming kernel (bound by the read of W, 2 V d bytes), 64 the "
+                "two-part streaming kernel, larger shapes the tiled MFMA kernel:", "",
                 "| shape | fused ms | fused TFLOP/s | % of 2.5 PFLOP/s | W read TB/s | GEMM ms | pass ms | unfused TFLOP/s | logits not stored |",
                 "|---|---|---|---|---|---|---|---|---|"]
         for r in lm:
