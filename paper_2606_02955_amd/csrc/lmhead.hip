@@ -8,6 +8,15 @@
 // the per-position outputs and the selection are then those of
 // fdllm_confidence / fdllm_decode_step (Sec. 3 "Notation"; Alg. 1).
 //
+// Three plans, by the number of positions N = B L:
+//   N <= 32     k_lm_stream: W streamed once, hidden operands in registers,
+//               logits folded in the kernel (HBM-bound);
+//   N <= 64     k_lm_kstream + k_lm_ksum: the same with the hidden dimension
+//               split over two workgroups, partial logits in the workspace;
+//   otherwise   k_lm_partial: MFMA tiles of 256 positions x 256 rows
+//               (bound by the matrix cores at large N);
+// each followed by k_lm_finish, which combines the per-split states.
+//
 // Main loop of the partial kernel: a workgroup of 8 waves owns 256 candidate
 // positions x 256 vocabulary rows per tile; the hidden dimension streams in
 // stages of 64 elements (128 bytes of every weight and hidden row, so each
