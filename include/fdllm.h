@@ -194,9 +194,11 @@ fdllm_status fdllm_decode_step(const void* logits, fdllm_dtype dtype, int B, int
  * ---------------------------------------------------------------------------
  * The logits of candidate position (b, i) are l_v = sum_k h[b,i,k] W[v,k],
  * formed on the matrix cores with float32 accumulation (bf16 operands) and
- * folded into the online (max, sum, argmax) of the vocabulary pass tile by
- * tile; no logit is stored.  From the logits on, the outputs are those of
- * fdllm_confidence (token, conf, eps, lse; defaults for non-candidates).
+ * folded into the online (max, sum, argmax) of the vocabulary pass; no full
+ * logit row is stored (for 33..64 positions the two halves of the hidden
+ * dimension's partial logits pass through the workspace, 2 x 64 x V floats).
+ * From the logits on, the outputs are those of fdllm_confidence (token,
+ * conf, eps, lse; defaults for non-candidates).
  *   hidden [B, L, d] bf16, 16-byte aligned (in): final hidden states;
  *   weight [V, d] bf16, 16-byte aligned (in): output embedding, row v for token v;
  *   d: a multiple of 64, hidden at most 4 GiB (B*L*d*2 < 2^32 bytes) and
