@@ -178,7 +178,10 @@ fdllm_status fdllm_reveal(const uint8_t* commit, const int32_t* tokens, int32_t*
  *   outputs (NULL to skip), with the meanings above.
  *   workspace: device memory of at least fdllm_workspace_size() bytes
  *   (may be NULL when that size is 0); its contents need no initialisation
- *   and are scratch between calls.
+ *   and are scratch between calls.  With tokens, conf and eps all given a
+ *   smaller workspace (or NULL) is accepted: the results are the same, but a
+ *   small batch of blocks of at most 64 positions then streams each row
+ *   from one workgroup instead of several.
  */
 fdllm_status fdllm_decode_step(const void* logits, fdllm_dtype dtype, int B, int L, int V,
                                uint8_t* mask, const int32_t* block_start, const int32_t* block_end,

@@ -216,7 +216,7 @@ def fdllm_decode_step(logits, mask, block_start, block_end, x, selector: str, pa
     ws_ptr, ws_bytes = None, 0
     if workspace is not None:
         ws_ptr, ws_bytes = _ptr(workspace, name="workspace"), workspace.numel() * workspace.element_size()
-    elif need and (tokens is None or conf is None or eps is None):
+    elif need:
         workspace = torch.empty(need, dtype=torch.uint8, device=logits.device)
         ws_ptr, ws_bytes = _ptr(workspace), need
     st = load().fdllm_decode_step(

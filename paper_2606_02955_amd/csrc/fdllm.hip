@@ -253,6 +253,25 @@ struct SplitShape {
   static constexpr int kThreads = kWaves * kWave;
 };
 
+// A row's S wave partials combined in part order; every plan that splits a
+// row S ways goes through this, so they all give the same bits.
+template <int S>
+__device__ __forceinline__ RowResult combine_parts(const WavePartial* part) {
+  float M = part[0].m;
+#pragma unroll
+  for (int q = 1; q < S; ++q) M = fmaxf(M, part[q].m);
+  const float K = exp_ref(M);
+  double Ssum = 0.0;
+  int first = 0x7fffffff;
+#pragma unroll
+  for (int q = 0; q < S; ++q) {
+    const WavePartial pq = part[q];
+    Ssum += rescale(pq.S, pq.K, K);
+    if (pq.m == M) first = min(first, pq.first);
+  }
+  return finish_row(M, K, Ssum, first);
+}
+
 template <class Vec, int U, int S>
 __global__ void __launch_bounds__(SplitShape<S>::kThreads)
 k_confidence(const typename Vec::Raw* __restrict__ logits, int B, int L, int nvec,
@@ -285,24 +304,35 @@ k_confidence(const typename Vec::Raw* __restrict__ logits, int B, int L, int nve
     store_default(out, (size_t)slot);
     return;
   }
-  float M = wp.m, K = wp.K;
-  double Ssum = wp.S;
-  int first = wp.first;
-  if constexpr (S > 1) {
-    M = part[rloc * S].m;
-#pragma unroll
-    for (int q = 1; q < S; ++q) M = fmaxf(M, part[rloc * S + q].m);
-    K = exp_ref(M);
-    Ssum = 0.0;
-    first = 0x7fffffff;
-#pragma unroll
-    for (int q = 0; q < S; ++q) {
-      const WavePartial& pq = part[rloc * S + q];
-      Ssum += rescale(pq.S, pq.K, K);
-      if (pq.m == M) first = min(first, pq.first);
-    }
+  if constexpr (S > 1)
+    store_row(out, (size_t)slot, combine_parts<S>(&part[rloc * S]));
+  else
+    store_row(out, (size_t)slot, finish_row(wp.m, wp.K, wp.S, wp.first));
+}
+
+// The same pass with a row's S parts spread over S / 4 workgroups of 4 waves
+// (more CUs stream the few rows of a small batch); each wave's partial goes
+// to parts[slot][w], combined by the select kernel.  Non-candidates get their
+// defaults here.
+template <class Vec, int U, int S>
+__global__ void __launch_bounds__(256)
+k_confidence_parts(const typename Vec::Raw* __restrict__ logits, int B, int L, int nvec,
+                   const uint8_t* __restrict__ mask, const int32_t* __restrict__ bstart,
+                   const int32_t* __restrict__ bend, RowOut out, WavePartial* __restrict__ parts) {
+  constexpr int P = S / 4;                                  // workgroups per slot
+  const int wave = threadIdx.x / kWave;
+  const int lane = threadIdx.x % kWave;
+  const long long slot = blockIdx.x / P;
+  const int w = (int)(blockIdx.x % P) * 4 + wave;           // part of the row
+  const int b = (int)(slot / L), i = (int)(slot % L);
+  const int s = bstart[b], e = bend[b];
+  const bool cand = window_ok(s, e, L) && i >= s && i < e && mask[slot] != 0;
+  if (!cand) {
+    if (w == 0 && lane == 0) store_default(out, (size_t)slot);
+    return;
   }
-  store_row(out, (size_t)slot, finish_row(M, K, Ssum, first));
+  const WavePartial wp = row_pass<Vec, U, S>(logits + slot * (long long)nvec, nvec, w);
+  if (lane == 0) parts[slot * S + w] = wp;
 }
 
 // ---------------------------------------------------------------------------
@@ -557,8 +587,11 @@ __device__ __forceinline__ void select_block_wave(const SelectIO& io, size_t row
 
 // Rows of at most 64 positions: one wavefront per block, four blocks per
 // workgroup.
-template <int R, bool Robust>
-__global__ void __launch_bounds__(256) k_select(SelectIO io, int B, int L, float param) {
+// PS > 0: the candidates' per-position outputs are first formed from their
+// PS wave partials (k_confidence_parts), each by the lane that selects it.
+template <int R, bool Robust, int PS>
+__global__ void __launch_bounds__(256) k_select(SelectIO io, int B, int L, float param,
+                                                const WavePartial* __restrict__ parts, RowOut out) {
   const int lane = threadIdx.x % kWave;
   const int b = blockIdx.x * 4 + threadIdx.x / kWave;
   if (b >= B) return;
@@ -566,6 +599,10 @@ __global__ void __launch_bounds__(256) k_select(SelectIO io, int B, int L, float
   const int s = io.bstart[b], e_end = io.bend[b];
   const bool ok = window_ok(s, e_end, L);
   const int len = ok ? e_end - s : 0;
+  if constexpr (PS > 0) {
+    const size_t i = row + (size_t)(s + lane);
+    if (lane < len && io.mask[i] != 0) store_row(out, i, combine_parts<PS>(parts + i * PS));
+  }
   if (io.commit) {
     // every entry of row b written once: window slots by their lane, the rest zero
     for (int q = lane; q < L; q += kWave)
@@ -820,6 +857,7 @@ __global__ void __launch_bounds__(256) k_reveal(const uint8_t* __restrict__ comm
 struct Plan {
   bool fused;   // one workgroup per sequence, selection in the same kernel
   int split;    // wavefronts per row in the confidence kernel
+  int parts;    // decode step with a workspace: split over split / 4 workgroups (0: no)
 };
 
 constexpr int kFusedMinB = 128;
@@ -837,6 +875,9 @@ static Plan make_plan(int B, int L, int V, fdllm_dtype dt) {
     const long long max_split = row_bytes / (16LL * kWave * 8);
     const long long slots = (long long)B * win;
     while (p.split < 16 && 2LL * p.split <= max_split && slots * p.split < kTargetWaves) p.split <<= 1;
+    // a row split 8 or 16 ways fills one CU; blocks of at most one wavefront
+    // can take their rows' parts from several workgroups instead
+    if (L <= kWaveBlock && p.split >= 8) p.parts = p.split;
   }
   return p;
 }
@@ -873,6 +914,41 @@ static hipError_t launch_confidence_t(const void* logits, int B, int L, int nvec
   return hipGetLastError();
 }
 
+template <class Vec>
+static hipError_t launch_confidence_parts_t(const void* logits, int B, int L, int nvec, int split,
+                                            const uint8_t* mask, const int32_t* bs,
+                                            const int32_t* be, RowOut out, WavePartial* parts,
+                                            hipStream_t st) {
+  const long long nslots = (long long)B * L;
+  const auto* lg = (const typename Vec::Raw*)logits;
+  const dim3 grid((unsigned)(nslots * (split / 4))), block(256);
+  if (split == 8)
+    hipLaunchKernelGGL((k_confidence_parts<Vec, Vec::kU, 8>), grid, block, 0, st, lg, B, L, nvec,
+                       mask, bs, be, out, parts);
+  else if (split == 16)
+    hipLaunchKernelGGL((k_confidence_parts<Vec, Vec::kU, 16>), grid, block, 0, st, lg, B, L, nvec,
+                       mask, bs, be, out, parts);
+  else
+    return hipErrorInvalidValue;
+  return hipGetLastError();
+}
+
+static hipError_t launch_confidence_parts(const void* logits, fdllm_dtype dt, int B, int L, int V,
+                                          int split, const uint8_t* mask, const int32_t* bs,
+                                          const int32_t* be, RowOut out, WavePartial* parts,
+                                          hipStream_t st) {
+  if (vec_path(logits, V, dt)) {
+    if (dt == FDLLM_BF16)
+      return launch_confidence_parts_t<VecBf16x8>(logits, B, L, V / 8, split, mask, bs, be, out,
+                                                  parts, st);
+    return launch_confidence_parts_t<VecF32x4>(logits, B, L, V / 4, split, mask, bs, be, out, parts,
+                                               st);
+  }
+  if (dt == FDLLM_BF16)
+    return launch_confidence_parts_t<VecBf16x1>(logits, B, L, V, split, mask, bs, be, out, parts, st);
+  return launch_confidence_parts_t<VecF32x1>(logits, B, L, V, split, mask, bs, be, out, parts, st);
+}
+
 static hipError_t launch_confidence(const void* logits, fdllm_dtype dt, int B, int L, int V,
                                     int split, const uint8_t* mask, const int32_t* bs,
                                     const int32_t* be, RowOut out, hipStream_t st) {
@@ -887,25 +963,36 @@ static hipError_t launch_confidence(const void* logits, fdllm_dtype dt, int B, i
 }
 
 template <int R, bool Robust>
-static void launch_select_t(const SelectIO& io, int B, int L, float param, hipStream_t st) {
+static void launch_select_t(const SelectIO& io, int B, int L, float param, hipStream_t st,
+                            int ps, const WavePartial* parts, RowOut out) {
   constexpr int kWideThreads = 256;
-  if (L <= kWaveBlock)
-    hipLaunchKernelGGL((k_select<R, Robust>), dim3((unsigned)((B + 3) / 4)), dim3(256), 0, st, io,
-                       B, L, param);
+  const dim3 g((unsigned)((B + 3) / 4)), t(256);
+  if (ps == 8)
+    hipLaunchKernelGGL((k_select<R, Robust, 8>), g, t, 0, st, io, B, L, param, parts, out);
+  else if (ps == 16)
+    hipLaunchKernelGGL((k_select<R, Robust, 16>), g, t, 0, st, io, B, L, param, parts, out);
+  else if (L <= kWaveBlock)
+    hipLaunchKernelGGL((k_select<R, Robust, 0>), g, t, 0, st, io, B, L, param, parts, out);
   else
     hipLaunchKernelGGL((k_select_wide<R, Robust, kWideThreads>), dim3((unsigned)B),
                        dim3(kWideThreads), 0, st, io, B, L, param);
 }
 
+// ps: 0, or the parts per row (8 or 16, L <= 64) left by k_confidence_parts
 hipError_t launch_select(fdllm_selector sel, const SelectIO& io, int B, int L, float param,
-                         hipStream_t st) {
+                         hipStream_t st, int ps, const WavePartial* parts, RowOut out) {
   switch (sel) {
-    case FDLLM_SEL_THRESHOLD: launch_select_t<kThreshold, false>(io, B, L, param, st); break;
-    case FDLLM_SEL_FACTOR: launch_select_t<kFactor, false>(io, B, L, param, st); break;
-    case FDLLM_SEL_ROBUST: launch_select_t<kProfile, true>(io, B, L, param, st); break;
-    default: launch_select_t<kProfile, false>(io, B, L, param, st); break;
+    case FDLLM_SEL_THRESHOLD: launch_select_t<kThreshold, false>(io, B, L, param, st, ps, parts, out); break;
+    case FDLLM_SEL_FACTOR: launch_select_t<kFactor, false>(io, B, L, param, st, ps, parts, out); break;
+    case FDLLM_SEL_ROBUST: launch_select_t<kProfile, true>(io, B, L, param, st, ps, parts, out); break;
+    default: launch_select_t<kProfile, false>(io, B, L, param, st, ps, parts, out); break;
   }
   return hipGetLastError();
+}
+
+hipError_t launch_select(fdllm_selector sel, const SelectIO& io, int B, int L, float param,
+                         hipStream_t st) {
+  return launch_select(sel, io, B, L, param, st, 0, nullptr, RowOut{});
 }
 
 template <class Vec, int R, bool Robust>
@@ -974,10 +1061,13 @@ static bool sizes_ok(int B, int L, int V) {
 }
 
 
+// tokens, conf and eps when the caller does not take them, then the rows'
+// wave partials of the parts plan
+static size_t out_bytes_for(int B, int L) { return 3 * align256((size_t)B * (size_t)L * 4); }
 static size_t workspace_bytes_for(int B, int L, const Plan& p) {
   if (p.fused) return 0;
   const size_t n = (size_t)B * (size_t)L;
-  return 3 * align256(n * 4);
+  return out_bytes_for(B, L) + (p.parts ? align256(n * p.parts * sizeof(WavePartial)) : 0);
 }
 
 }  // namespace fdllm
@@ -1109,16 +1199,25 @@ fdllm_status fdllm_decode_step(const void* logits, fdllm_dtype dtype, int B, int
   // two kernels: confidence into the caller's arrays or the workspace, then select+reveal
   const size_t n = (size_t)B * (size_t)L;
   const bool need_ws = !tokens || !conf || !eps;
-  if (need_ws && (!workspace || workspace_bytes < workspace_bytes_for(B, L, p)))
-    return FDLLM_ERR_WORKSPACE;
+  if (need_ws && (!workspace || workspace_bytes < out_bytes_for(B, L))) return FDLLM_ERR_WORKSPACE;
   char* ws = (char*)workspace;
   if (!tokens) tokens = (int32_t*)ws;
   if (!conf) conf = (float*)(ws + align256(n * 4));
   if (!eps) eps = (float*)(ws + 2 * align256(n * 4));
   out = RowOut{tokens, conf, eps, lse};
+  SelectIO io{conf, eps, mask, block_start, block_end, commit, n_commit, tokens, x, etain};
+  if (p.parts && workspace && workspace_bytes >= workspace_bytes_for(B, L, p)) {
+    // the rows' parts from several workgroups each, combined by the selection
+    // (the same bits as the single-workgroup rows of fdllm_confidence)
+    WavePartial* parts = (WavePartial*)(ws + out_bytes_for(B, L));
+    err = launch_confidence_parts(logits, dtype, B, L, V, p.parts, mask, block_start, block_end, out,
+                                  parts, st);
+    if (err != hipSuccess) return FDLLM_ERR_HIP;
+    err = launch_select(sel, io, B, L, param, st, p.parts, parts, out);
+    return err == hipSuccess ? FDLLM_OK : FDLLM_ERR_HIP;
+  }
   err = launch_confidence(logits, dtype, B, L, V, p.split, mask, block_start, block_end, out, st);
   if (err != hipSuccess) return FDLLM_ERR_HIP;
-  SelectIO io{conf, eps, mask, block_start, block_end, commit, n_commit, tokens, x, etain};
   err = launch_select(sel, io, B, L, param, st);
   return err == hipSuccess ? FDLLM_OK : FDLLM_ERR_HIP;
 }

@@ -47,6 +47,8 @@ SMALL = [
     (130, 8, 520, torch.bfloat16, None),      # enough sequences for the fused plan
     (160, 12, 1024, torch.float32, 12),
     (129, 3, 7, torch.bfloat16, None),        # fused plan, scalar path
+    (2, 24, 40000, torch.bfloat16, 24),       # rows split 8 ways (decode: two workgroups per row)
+    (1, 20, 70001, torch.bfloat16, None),     # split 16 ways, scalar path
 ]
 
 # blocks beyond one wavefront (block-size ablation): workgroup selection
@@ -289,3 +291,28 @@ def test_wide_flat_block_profile_equals_factor(gpu, B):
         assert (op["n_commit"] == n).all() and n == want, (n, want)
         # ties go to the lower positions: the first n* slots commit
         assert int(op["commit"][:, :n].sum()) == B * n and int(op["commit"][:, n:].sum()) == 0
+
+
+@pytest.mark.parametrize("B,L,V,dt,window", [(2, 17, 126464, torch.float32, 17),
+                                              (2, 24, 40000, torch.bfloat16, 24)])
+def test_decode_step_row_parts_match_single_workgroup(gpu, B, L, V, dt, window):
+    """A small batch's rows streamed by several workgroups (the workspace holds
+    their partials) give the same bits as one workgroup per row (no workspace)."""
+    inp = _case(B, L, V, dt, window, seed=B + L + V)
+    say(f"[decode parts vs single workgroup] {inp.name}")
+    outs = []
+    for ws in (None, torch.empty(1, dtype=torch.uint8, device="cuda")):
+        mask, x = inp.mask.clone(), inp.x.clone()
+        o = {"tokens": torch.full((B, L), -7, dtype=torch.int32, device="cuda"),
+             "conf": torch.full((B, L), -7.0, device="cuda"),
+             "eps": torch.full((B, L), -7.0, device="cuda"),
+             "lse": torch.full((B, L), -7.0, device="cuda"),
+             "commit": torch.full((B, L), 9, dtype=torch.uint8, device="cuda"),
+             "n_commit": torch.full((B,), -9, dtype=torch.int32, device="cuda")}
+        gpu.fdllm_decode_step(inp.logits, mask, inp.start, inp.end, x, "profile", 1.0, workspace=ws, **o)
+        torch.cuda.synchronize()
+        outs.append((mask, x, o))
+    (m1, x1, o1), (m2, x2, o2) = outs
+    assert torch.equal(m1, m2) and torch.equal(x1, x2)
+    for k in o1:
+        assert torch.equal(o1[k].view(torch.uint8), o2[k].view(torch.uint8)), k
