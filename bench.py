@@ -259,7 +259,7 @@ def per_workload_report(fd, torch, workloads, dev, stream_gbps, reps):
     torch.cuda.empty_cache()
     # whole simulated generations (B=8 of 256), one per selector
     for sel, p in sels[workloads.GENERATION]:
-        gen = workloads.SimulatedGeneration(2, device=dev)
+        gen = workloads.SimulatedGeneration(workloads.GENERATION, device=dev)
         nc = torch.empty((gen.B,), dtype=torch.int32, device=dev)
         steps, commits, positions, ktime, ws = 0, 0, 0, 0.0, None
         e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
@@ -275,7 +275,8 @@ def per_workload_report(fd, torch, workloads, dev, stream_gbps, reps):
             commits += int(nc.clamp(min=0).sum())
             steps += 1
         nbytes = positions * gen.V * 2
-        rows.append(_row(2, "B=8 gen 256 in blocks of 32, V=126464 bf16 (whole generation)",
+        rows.append(_row(workloads.RECIPE_NAMES[workloads.GENERATION],
+                         "B=8 gen 256 in blocks of 32, V=126464 bf16 (whole generation)",
                          f"{sel}({p})", positions / steps, nbytes / steps, ktime / steps, None,
                          stream_gbps, {"steps": steps, "commits_per_step": commits / steps,
                                        "note": "hot: each step's rows were just written"}))
@@ -375,8 +376,9 @@ def per_workload_markdown(rows, stress, stream_gbps, cmd) -> str:
            f"Read-only stream reference (`fdllm_stream_read` over the 8.29 GB logits buffer): "
            f"{stream_gbps:.0f} GB/s.  Kernel times are HIP-event averages of `fdllm_decode_step`; "
            "`cold` overwrites a 512 MB buffer before every step (evicting L2 and the Infinity "
-           "Cache), `hot` does not.  The per-step traffic of the B=8 generation is 8x32 rows, so its steps "
-           "are launch-bound.", "",
+           "Cache), `hot` does not (with no long kernel queued ahead, a hot step's event window also holds "
+           "the host's launch gaps between its kernels).  The per-step traffic of the B=8 generation is "
+           "8x32 rows, so its steps are launch-bound.", "",
            "| workload | shape | selector | positions/step | kernel ms (cold) | kernel ms (hot) | "
            "positions/s | logits GB/s | % of 8 TB/s | % of stream | commits |",
            "|---|---|---|---|---|---|---|---|---|---|---|"]
@@ -385,11 +387,14 @@ def per_workload_markdown(rows, stress, stream_gbps, cmd) -> str:
     rows = [r for r in rows if r["workload"] not in ("device-loop", "lmhead")]
     for r in rows + stress:
         hot = f"{r['kernel_ms_hot']:.4f}" if r["kernel_ms_hot"] is not None else "—"
+        cold = f"{r['kernel_ms_cold']:.4f}"
+        if str(r.get("note", "")).startswith("hot"):      # steps timed right after their rows were written
+            cold, hot = "—", cold
         commits = (f"{r['commits_per_step']:.2f}/step, {r['steps']} steps" if "steps" in r
                    else f"{r.get('mean_commits_per_block', 0):.2f}/block")
         fs = f"{100 * r['frac_of_stream']:.1f}" if r["frac_of_stream"] else "—"
         out.append(f"| {r['workload']} | {r['shape']} | {r['selector']} | {r['positions_per_step']:.0f} | "
-                   f"{r['kernel_ms_cold']:.4f} | {hot} | {r['positions_per_s']:.4g} | "
+                   f"{cold} | {hot} | {r['positions_per_s']:.4g} | "
                    f"{r['logits_GBps']:.0f} | {100 * r['frac_of_peak']:.1f} | {fs} | {commits} |")
     if loop:
         out += ["", "Whole generations in the device-resident loop (`fdllm_generation_run`: "
