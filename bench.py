@@ -422,6 +422,44 @@ def per_workload_markdown(rows, stress, stream_gbps, cmd) -> str:
     return "\n".join(out) + "\n"
 
 
+def lmhead_only(n, steps, warmup):
+    """Times fdllm_lmhead_confidence on n positions (one sequence's block of
+    up to 32, or n / 32 of them) with random bf16 hidden states and output
+    embedding; prints one JSON line."""
+    import torch
+    import paper_2606_02955_amd as fd
+    import workloads
+    fd.load()
+    dev = torch.device("cuda", 0)
+    d, V = 4096, workloads.V_LLADA
+    L = min(n, 32)
+    B = (n + L - 1) // L
+    g = torch.Generator(device=dev).manual_seed(2606)
+    weight = (torch.randn((V, d), generator=g, device=dev) / 64).to(torch.bfloat16)
+    hid = torch.randn((B, L, d), generator=g, device=dev).to(torch.bfloat16)
+    mk = torch.ones((B, L), dtype=torch.uint8, device=dev)
+    mk.view(-1)[n:] = 0
+    st_ = torch.zeros(B, dtype=torch.int32, device=dev)
+    en_ = torch.full((B,), L, dtype=torch.int32, device=dev)
+    tok = torch.empty((B, L), dtype=torch.int32, device=dev)
+    cf = torch.empty((B, L), device=dev)
+    ws = fd.fdllm_lmhead_confidence(hid, weight, mk, st_, en_, tok, cf)
+    for _ in range(warmup):
+        fd.fdllm_lmhead_confidence(hid, weight, mk, st_, en_, tok, cf, workspace=ws)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(steps):
+        fd.fdllm_lmhead_confidence(hid, weight, mk, st_, en_, tok, cf, workspace=ws)
+    e1.record()
+    torch.cuda.synchronize()
+    t = e0.elapsed_time(e1) * 1e-3 / steps
+    print(json.dumps({"metric": "fused LM head + vocabulary pass, one GPU", "value": n / t,
+                      "unit": "positions/s", "ms_per_call": 1e3 * t, "steps": steps, "warmup": warmup,
+                      "positions": n, "B": B, "L": L, "d": d, "V": V, "dtype": "bf16",
+                      "W_read_TBps": 2.0 * V * d / t / 1e12, "data": "synthetic"}), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -439,6 +477,9 @@ def main():
     ap.add_argument("--per-workload-md", default=None, help="write the per-workload table here")
     ap.add_argument("--copy-calibration-mb", type=int, default=1024,
                     help="size of a plain device copy timed (and counted by rocprofv3) for reference")
+    ap.add_argument("--lmhead-positions", type=int, default=0,
+                    help="instead: time only the fused LM head on this many positions "
+                         "(d=4096, V=126464 bf16; one JSON line)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py measures one GPU only; --gpus {args.gpus} is not supported "
@@ -446,6 +487,9 @@ def main():
               file=sys.stderr)
         sys.exit(2)
     param = args.param if args.param is not None else (0.9 if args.selector == "threshold" else 1.0)
+    if args.lmhead_positions > 0:
+        lmhead_only(args.lmhead_positions, args.steps, args.warmup)
+        return
 
     crew, crew_note = None, None
     if not args.no_cpu_baseline:
