@@ -20,11 +20,12 @@
 // Main loop of the partial kernel: a workgroup of 8 waves owns 256 candidate
 // positions x 256 vocabulary rows per tile; the hidden dimension streams in
 // stages of 64 elements (128 bytes of every weight and hidden row, so each
-// load uses whole cache lines; 64 KiB per stage) that buffer_load ... lds
-// writes straight into LDS, two stages resident.  One barrier per stage;
-// each wave's 64 MFMAs of a stage are interleaved with the reads of the next
-// half stage's operands, and the second half with the loads of the stage
-// after next.
+// load uses whole cache lines; 32 KiB of weights and 32 KiB of hidden states
+// per stage) that buffer_load ... lds writes straight into LDS, three weight
+// and two hidden stages resident (160 KiB).  One barrier per stage; each
+// wave's 64 MFMAs of a stage are interleaved with the reads of the next half
+// stage's operands, and the second half with the loads of the hidden part of
+// the stage after next and the weight part of the one after that.
 #include <hip/hip_runtime.h>
 
 #include <stdint.h>
@@ -48,7 +49,6 @@ constexpr int kLmWaves = 8;                    // waves per workgroup
 constexpr int kLmVt = 256;                     // vocabulary rows per tile (MFMA A operand)
 constexpr int kLmPt = 256;                     // positions per workgroup (MFMA B operand)
 constexpr int kLmBK = 64;                      // hidden-dimension elements per LDS stage
-constexpr int kLmNBuf = 2;                     // stages resident in LDS
 constexpr int kLmThreads = kLmWaves * kWave;
 constexpr int kLmRows = kLmPt;                 // candidate rows per workgroup
 constexpr int kLmCols = kLmVt;                 // vocabulary columns per tile
@@ -144,21 +144,25 @@ __device__ __forceinline__ void lm_combine(LmState& st, float M2, float K2, doub
 // ---- LDS-DMA main loop -----------------------------------------------------
 // Stages of kLmBK hidden elements: 256 weight rows and 256 hidden rows of
 // kLmBK * 2 bytes each, written by buffer_load ... lds (each lane of a wave
-// instruction fills the next 16 bytes of LDS).  The stage after next is
-// loaded into the buffer of the stage just read, in the second half of the
-// current stage.  Rows are stored unpadded; the 16-byte vector s of row r
+// instruction fills the next 16 bytes of LDS).  The weight part runs one
+// stage further ahead (three buffers; it comes from HBM or the Infinity
+// Cache) than the hidden part (two buffers; mostly L2 hits); both are loaded
+// into the buffers of the stage just read, in the second half of the current
+// stage.  Rows are stored unpadded; the 16-byte vector s of row r
 // sits in slot s ^ lm_swz(r).  lm_swz was chosen from LDS bank-conflict
 // counter measurements of ds_read_b128 patterns on gfx950: with it the
 // operand reads (lane l: row l % 16, vector 4 h + l / 16) are conflict-free.
 constexpr int kLmSlots = kLmBK / 8;                       // 16-byte vectors per row and stage
 constexpr int kLmRowBytes = kLmBK * 2;
 constexpr int kLmWBytes = kLmVt * kLmRowBytes;            // weight part of a stage
-constexpr int kLmStageBytes = (kLmVt + kLmPt) * kLmRowBytes;
 constexpr int kLmDmaRows = kWave / kLmSlots;              // rows per wave-wide load
 constexpr int kLmWDma = kLmVt / kLmDmaRows / kLmWaves;    // weight loads per wave and stage
 constexpr int kLmHDma = kLmPt / kLmDmaRows / kLmWaves;
 constexpr int kLmDmaPerStage = kLmWDma + kLmHDma;
-constexpr size_t kLmLdsBytes = (size_t)kLmNBuf * kLmStageBytes;
+constexpr int kLmWBuf = 3, kLmHBuf = 2;                  // weight and hidden stages resident
+constexpr int kLmHBytes = kLmPt * kLmRowBytes;            // hidden part of a stage
+constexpr int kLmHOff = kLmWBuf * kLmWBytes;              // hidden buffers after the weight ones
+constexpr size_t kLmLdsBytes = (size_t)kLmWBuf * kLmWBytes + (size_t)kLmHBuf * kLmHBytes;
 static_assert(kLmWDma == 4 && kLmHDma == 4, "the interleaved schedule issues four loads of each");
 
 __device__ __forceinline__ int lm_swz(int r) { return (r & 1) | ((r >> 1) & 2) | ((r << 1) & 4); }
@@ -205,7 +209,8 @@ __device__ __forceinline__ void lm_sync() {
 // (into a buffer nobody reads any more), so every stage issues the same
 // number of loads.
 struct LmProducer {
-  int tile, ks, left, buf;
+  int tile, ks, left, buf;        // weight stages
+  int hks, hleft, hbuf;           // hidden stages (one behind)
   i32x4 wr, hr;
   uint32_t w_voff[kLmWDma], h_voff[kLmHDma];
   uint32_t lds_w[kLmWDma], lds_h[kLmHDma];   // wave's LDS offsets within a stage
@@ -254,6 +259,9 @@ k_lm_partial(const uint16_t* __restrict__ hidden, const uint16_t* __restrict__ w
   pr.ks = 0;
   pr.left = (t_end - t_begin) * nks;
   pr.buf = 0;
+  pr.hks = 0;
+  pr.hleft = pr.left;
+  pr.hbuf = 0;
   pr.hr = lm_rsrc(hidden, hid_bytes);
   {
     const int lr = lane / kLmSlots, ls = lane % kLmSlots;
@@ -262,7 +270,7 @@ k_lm_partial(const uint16_t* __restrict__ hidden, const uint16_t* __restrict__ w
       const int r = (wave * kLmHDma + j) * kLmDmaRows + lr;
       const int q = p0 + r < nrows ? p0 + r : p0;       // past the end: repeat the first row
       pr.h_voff[j] = (uint32_t)rows[q] * (uint32_t)d * 2u + (uint32_t)((ls ^ lm_swz(r)) * 16);
-      pr.lds_h[j] = (uint32_t)(kLmWBytes + (wave * kLmHDma + j) * kLmDmaRows * kLmRowBytes);
+      pr.lds_h[j] = (uint32_t)(kLmHOff + (wave * kLmHDma + j) * kLmDmaRows * kLmRowBytes);
     }
 #pragma unroll
     for (int j = 0; j < kLmWDma; ++j)
@@ -270,16 +278,17 @@ k_lm_partial(const uint16_t* __restrict__ hidden, const uint16_t* __restrict__ w
   }
   lm_tile_setup(pr, weight, t_begin, V, d, lane, wave);
 
-  // the loads of the producer's stage: W j (j < 4) or H j - 4
+  // the loads of the producers' stages: H j (j < 4) of the hidden producer,
+  // then W j - 4 of the weight producer (one stage ahead)
   auto dma = [&](int j) {
-    const uint32_t sb = lds0 + (uint32_t)pr.buf * kLmStageBytes;
-    const int soff = pr.ks * kLmRowBytes;
-    if (j < kLmWDma)
-      lm_dma(pr.wr, sb + pr.lds_w[j], pr.w_voff[j], soff);
+    if (j < kLmHDma)
+      lm_dma(pr.hr, lds0 + (uint32_t)pr.hbuf * kLmHBytes + pr.lds_h[j], pr.h_voff[j],
+             pr.hks * kLmRowBytes);
     else
-      lm_dma(pr.hr, sb + pr.lds_h[j - kLmWDma], pr.h_voff[j - kLmWDma], soff);
+      lm_dma(pr.wr, lds0 + (uint32_t)pr.buf * kLmWBytes + pr.lds_w[j - kLmHDma],
+             pr.w_voff[j - kLmHDma], pr.ks * kLmRowBytes);
   };
-  auto advance = [&]() {
+  auto advance_w = [&]() {
     if (pr.left > 1) {
       --pr.left;
       if (++pr.ks == nks) {
@@ -288,7 +297,14 @@ k_lm_partial(const uint16_t* __restrict__ hidden, const uint16_t* __restrict__ w
         lm_tile_setup(pr, weight, t_begin + pr.tile, V, d, lane, wave);
       }
     }
-    pr.buf = pr.buf + 1 == kLmNBuf ? 0 : pr.buf + 1;
+    pr.buf = pr.buf + 1 == kLmWBuf ? 0 : pr.buf + 1;
+  };
+  auto advance_h = [&]() {
+    if (pr.hleft > 1) {
+      --pr.hleft;
+      if (++pr.hks == nks) pr.hks = 0;
+    }
+    pr.hbuf ^= 1;
   };
 
   // operand addresses of this lane: row l % 16 of a 16-row block, 16-byte
@@ -298,7 +314,7 @@ k_lm_partial(const uint16_t* __restrict__ hidden, const uint16_t* __restrict__ w
   for (int h = 0; h < 2; ++h) {
     const uint32_t slot = (uint32_t)(((4 * h + lane / 16) ^ lm_swz(lane % 16)) * 16);
     a_addr[h] = (uint32_t)((128 * vw + lane % 16) * kLmRowBytes) + slot;
-    b_addr[h] = (uint32_t)(kLmWBytes + (64 * pw + lane % 16) * kLmRowBytes) + slot;
+    b_addr[h] = (uint32_t)(kLmHOff + (64 * pw + lane % 16) * kLmRowBytes) + slot;
   }
   auto lds_at = [&](uint32_t a) -> bf16x8 {
     return *reinterpret_cast<const bf16x8*>(lm_lds + (a - lds0));
@@ -335,19 +351,24 @@ k_lm_partial(const uint16_t* __restrict__ hidden, const uint16_t* __restrict__ w
     fa[7] = na7;
   };
 
-  // prologue: both buffers' stages in flight, then wait for the first
-  for (int s = 0; s < kLmNBuf; ++s) {
+  // prologue: stages 0 and 1 of both, and the weight part of stage 2, in
+  // flight (in this order), then wait for stage 0
+  for (int s = 0; s < 2; ++s) {
 #pragma unroll
     for (int j = 0; j < kLmDmaPerStage; ++j) dma(j);
-    advance();
+    advance_h();
+    advance_w();
   }
-  lm_sync<kLmDmaPerStage>();
+#pragma unroll
+  for (int j = kLmHDma; j < kLmDmaPerStage; ++j) dma(j);
+  advance_w();
+  lm_sync<kLmDmaPerStage + kLmWDma>();
 #pragma unroll
   for (int ni = 0; ni < 4; ++ni) fb[ni] = lds_at(lds0 + b_addr[0] + ni * 16 * kLmRowBytes);
 #pragma unroll
   for (int mi = 0; mi < 8; ++mi) fa[mi] = lds_at(lds0 + a_addr[0] + mi * 16 * kLmRowBytes);
 
-  int cbuf = 0;
+  int wbuf = 0, hbuf = 0;     // buffers of the stage being consumed
   for (int t = t_begin; t < t_end; ++t) {
 #pragma unroll
     for (int mi = 0; mi < 8; ++mi)
@@ -356,22 +377,25 @@ k_lm_partial(const uint16_t* __restrict__ hidden, const uint16_t* __restrict__ w
 #pragma unroll
         for (int i = 0; i < 4; ++i) acc[mi][ni][i] = 0.0f;
     for (int ks = 0; ks < nks; ++ks) {
-      const uint32_t cb = lds0 + (uint32_t)cbuf * kLmStageBytes;
-      const int nbuf = cbuf ^ 1;
-      const uint32_t nb = lds0 + (uint32_t)nbuf * kLmStageBytes;
+      const uint32_t cw = lds0 + (uint32_t)wbuf * kLmWBytes, ch = lds0 + (uint32_t)hbuf * kLmHBytes;
+      const int nwbuf = wbuf + 1 == kLmWBuf ? 0 : wbuf + 1, nhbuf = hbuf ^ 1;
+      const uint32_t nw = lds0 + (uint32_t)nwbuf * kLmWBytes, nh = lds0 + (uint32_t)nhbuf * kLmHBytes;
       // first half: MFMAs on the stage's half 0, its half 1 read in between
       LM_FENCE();
-      half(cb + a_addr[1], cb + b_addr[1], false);
-      // every wave has read all of this stage's buffer, and the next stage
-      // (the only loads outstanding) has landed
+      half(cw + a_addr[1], ch + b_addr[1], false);
+      // every wave has read all of this stage's buffers, and the next stage
+      // has landed (only the weight part of the one after is outstanding)
       LM_FENCE();
-      lm_sync<0>();
-      // second half: MFMAs on half 1; the next stage's half 0 read and the
-      // stage after it loaded into this stage's buffer in between
-      half(nb + a_addr[0], nb + b_addr[0], true);
+      lm_sync<kLmWDma>();
+      // second half: MFMAs on half 1; the next stage's half 0 read, and the
+      // hidden part of the stage after next and the weight part of the one
+      // after that loaded into this stage's buffers, in between
+      half(nw + a_addr[0], nh + b_addr[0], true);
       LM_FENCE();
-      advance();
-      cbuf = nbuf;
+      advance_h();
+      advance_w();
+      wbuf = nwbuf;
+      hbuf = nhbuf;
     }
     const int base = t * kLmVt + 128 * vw + 4 * (lane / 16);
 #pragma unroll
@@ -999,7 +1023,7 @@ static bool lm_sizes_ok(int B, int L, int d, int V) {
   return (long long)B * L * d * 2 <= 0xffffffffLL && (long long)V * (d / 8) < 0x7fffffffLL;
 }
 
-// The partial kernels' dynamic LDS (128 and up to 144 KiB) is above the
+// The streaming and tiled kernels' dynamic LDS (up to 160 KiB) is above the
 // default limit; the limit is raised once per device, before the first launch
 // there.
 constexpr int kLmMaxDevices = 64;
