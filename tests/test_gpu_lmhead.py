@@ -38,12 +38,14 @@ CASES = [
     (1, 20, 512, 3001, "random", 20),
     (1, 32, 1536, 2000, "exact", 32),
     (4, 8, 1024, 2500, "exact", 5),          # several sequences, windows inside them
+    (1, 1, 512, 100, "exact", 1),            # a single position
     (1, 32, 64, 1000, "exact", 32),          # d not a multiple of 512: the tiled kernel
     # 33..64 positions, d a multiple of 1024: the k-split kernel
     (2, 32, 4096, 126464, "exact", 32),      # two sequences' blocks at LLaDA's sizes
     (1, 64, 1024, 3001, "random", 64),
     (2, 20, 3072, 999, "exact", 20),
     (1, 50, 4096, 700, "random", 50),        # fewer row blocks than workgroup groups
+    (1, 33, 2048, 1234, "random", 33),       # one position past a single block
     # more positions: the tiled kernel
     (4, 32, 2048, 5000, "exact", 32),
     (3, 40, 4096, 2000, "random", 40),
