@@ -272,6 +272,11 @@ __device__ __forceinline__ RowResult combine_parts(const WavePartial* part) {
   return finish_row(M, K, Ssum, first);
 }
 
+// Row group r of the grid handles the window-relative slot (b, q), q < W =
+// min(L, 64): the window positions q, q + W, ... of sequence b (one for a
+// window of at most W positions), and the defaults of the positions j = q,
+// q + W, ... of the whole row of L slots that lie outside the window.  So
+// only B W row groups are launched, however long the span L.
 template <class Vec, int U, int S>
 __global__ void __launch_bounds__(SplitShape<S>::kThreads)
 k_confidence(const typename Vec::Raw* __restrict__ logits, int B, int L, int nvec,
@@ -283,31 +288,46 @@ k_confidence(const typename Vec::Raw* __restrict__ logits, int B, int L, int nve
   const int lane = threadIdx.x % kWave;
   const int rloc = wave / S;
   const int w = wave % S;
-  const long long slot = (long long)blockIdx.x * Shape::kRows + rloc;
-  const long long nslots = (long long)B * L;
-  bool cand = false;
-  int b = 0, i = 0;
-  if (slot < nslots) {
-    b = (int)(slot / L);
-    i = (int)(slot % L);
-    const int s = bstart[b], e = bend[b];
-    cand = window_ok(s, e, L) && i >= s && i < e && mask[slot] != 0;
+  const int W = L < kWaveBlock ? L : kWaveBlock;
+  const long long vs = (long long)blockIdx.x * Shape::kRows + rloc;
+  const bool live = vs < (long long)B * W;
+  int b = 0, q = 0, s = 0, len = 0;
+  if (live) {
+    b = (int)(vs / W);
+    q = (int)(vs % W);
+    const int s0 = bstart[b], e0 = bend[b];
+    if (window_ok(s0, e0, L)) {
+      s = s0;
+      len = e0 - s0;
+    }
   }
-  WavePartial wp{};
-  if (cand) wp = row_pass<Vec, U, S>(logits + slot * (long long)nvec, nvec, w);
-  if constexpr (S > 1) {
-    if (lane == 0) part[wave] = wp;
-    __syncthreads();
+  const size_t row0 = (size_t)b * L;
+  if (live && w == 0 && lane == 0)
+    for (int j = q; j < L; j += W)
+      if (j < s || j >= s + len) store_default(out, row0 + j);
+  // the trip count depends on L only, so all row groups meet the same barriers
+  const int trips = (L + W - 1) / W;
+  for (int it = 0; it < trips; ++it) {
+    const int rel = q + it * W;
+    const bool inwin = live && rel < len;
+    const size_t slot = row0 + (size_t)(s + rel);
+    const bool cand = inwin && mask[slot] != 0;
+    WavePartial wp{};
+    if (cand) wp = row_pass<Vec, U, S>(logits + (long long)slot * nvec, nvec, w);
+    if constexpr (S > 1) {
+      if (lane == 0) part[wave] = wp;
+      __syncthreads();
+    }
+    if (w == 0 && lane == 0 && inwin) {
+      if (!cand)
+        store_default(out, slot);
+      else if constexpr (S > 1)
+        store_row(out, slot, combine_parts<S>(&part[rloc * S]));
+      else
+        store_row(out, slot, finish_row(wp.m, wp.K, wp.S, wp.first));
+    }
+    if constexpr (S > 1) __syncthreads();   // part[] is written again by the next trip
   }
-  if (w != 0 || lane != 0 || slot >= nslots) return;
-  if (!cand) {
-    store_default(out, (size_t)slot);
-    return;
-  }
-  if constexpr (S > 1)
-    store_row(out, (size_t)slot, combine_parts<S>(&part[rloc * S]));
-  else
-    store_row(out, (size_t)slot, finish_row(wp.m, wp.K, wp.S, wp.first));
 }
 
 // The same pass with a row's S parts spread over S / 4 workgroups of 4 waves
@@ -891,12 +911,12 @@ template <class Vec>
 static hipError_t launch_confidence_t(const void* logits, int B, int L, int nvec, int split,
                                       const uint8_t* mask, const int32_t* bs, const int32_t* be,
                                       RowOut out, hipStream_t st) {
-  const long long nslots = (long long)B * L;
+  const long long nvslots = (long long)B * (L < kWaveBlock ? L : kWaveBlock);   // window-relative
   const auto* lg = (const typename Vec::Raw*)logits;
 #define FDLLM_CONF_CASE(SPLIT)                                                                  \
   case SPLIT: {                                                                                 \
     using Sh = SplitShape<SPLIT>;                                                               \
-    const long long grid = (nslots + Sh::kRows - 1) / Sh::kRows;                                \
+    const long long grid = (nvslots + Sh::kRows - 1) / Sh::kRows;                               \
     hipLaunchKernelGGL((k_confidence<Vec, Vec::kU, SPLIT>), dim3((unsigned)grid), dim3(Sh::kThreads), \
                        0, st, lg, B, L, nvec, mask, bs, be, out);                               \
     break;                                                                                      \
