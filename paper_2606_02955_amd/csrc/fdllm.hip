@@ -305,8 +305,9 @@ k_confidence(const typename Vec::Raw* __restrict__ logits, int B, int L, int nve
   if (live && w == 0 && lane == 0)
     for (int j = q; j < L; j += W)
       if (j < s || j >= s + len) store_default(out, row0 + j);
-  // the trip count depends on L only, so all row groups meet the same barriers
-  const int trips = (L + W - 1) / W;
+  // trips over the window; where row groups of one workgroup meet barriers
+  // (S = 2: two row groups), a count that depends on L only
+  const int trips = (S == 1 || Shape::kRows == 1) ? (len - q + W - 1) / W : (L + W - 1) / W;
   for (int it = 0; it < trips; ++it) {
     const int rel = q + it * W;
     const bool inwin = live && rel < len;
