@@ -217,3 +217,32 @@ def test_lmhead_entry_points_check_arguments(lib):
     dargs[10] = 2
     dargs[9] = None
     assert lib.fdllm_lmhead_decode_step(*dargs) == fd.ERR_INVALID_ARG          # x missing
+
+
+def _ws(fn, *args):
+    n = ctypes.c_size_t(0)
+    assert fn(*args, ctypes.byref(n)) == 0
+    return n.value
+
+
+def test_workspace_sizes_follow_the_plans(lib):
+    """Host planning, seen through the workspace queries: small batches with
+    blocks of at most one wavefront reserve room for the rows' wave partials
+    (24 bytes each); the LM head's two-part plan (33..64 positions, d a
+    multiple of 1024) reserves the two halves' partial logits."""
+    V = 126464
+    # decode step: B=1, L=32 bf16 rows split 16 ways -> 32 x 16 partials
+    small = _ws(lib.fdllm_workspace_size, 1, 32, V, 0)
+    assert small >= 3 * 32 * 4 + 32 * 16 * 24
+    # a long span (L > 64) keeps single-workgroup rows: outputs only
+    assert _ws(lib.fdllm_workspace_size, 8, 256, V, 0) < 3 * 8 * 256 * 4 + 1024 * 3
+    # LM head: up to 32 positions need no partial logits
+    s32 = _ws(lib.fdllm_lmhead_workspace_size, 1, 32, 4096, V)
+    assert s32 < 4 << 20
+    # 64 positions: 2 halves x V x 64 float32 partial logits
+    s64 = _ws(lib.fdllm_lmhead_workspace_size, 2, 32, 4096, V)
+    assert s64 >= 2 * V * 64 * 4
+    # 64 positions with d not a multiple of 1024: the tiled plan, no partial logits
+    assert _ws(lib.fdllm_lmhead_workspace_size, 2, 32, 4032, V) < 2 * V * 64 * 4
+    # 65 positions: the tiled plan
+    assert _ws(lib.fdllm_lmhead_workspace_size, 1, 65, 4096, V) < 2 * V * 64 * 4
