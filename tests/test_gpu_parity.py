@@ -316,3 +316,44 @@ def test_decode_step_row_parts_match_single_workgroup(gpu, B, L, V, dt, window):
     assert torch.equal(m1, m2) and torch.equal(x1, x2)
     for k in o1:
         assert torch.equal(o1[k].view(torch.uint8), o2[k].view(torch.uint8)), k
+
+
+def _random_shapes(n, seed=2606):
+    """Seeded small-batch shapes: odd spans, windows above one wavefront, rows
+    long enough to be split, both dtypes."""
+    rng = np.random.default_rng(seed)
+    out = []
+    for k in range(n):
+        B = int(rng.integers(1, 7))
+        L = int(rng.choice([1, 7, 31, 64, 65, 130, 300]))
+        V = int(rng.choice([5, 129, 2047, 9000, 40000]))
+        dt = torch.bfloat16 if k % 2 == 0 else torch.float32
+        lo = 65 if (k % 3 == 0 and L > 64) else 1          # every third: beyond a wavefront
+        window = int(rng.integers(lo, min(L, 1024) + 1))
+        out.append((B, L, V, dt, window))
+    return out
+
+
+@pytest.mark.parametrize("B,L,V,dt,window", _random_shapes(12))
+def test_decode_step_random_shapes(gpu, B, L, V, dt, window):
+    """Random small-batch shapes through the two-kernel plans: the oracle's
+    selection, defaults outside the windows, and the same bits as
+    fdllm_confidence."""
+    inp = _case(B, L, V, dt, window, seed=B * 101 + L * 7 + V)
+    say(f"[decode random] {inp.name} window {window}")
+    m0, x0 = inp.mask.cpu().numpy(), inp.x.cpu().numpy()
+    start, end = inp.start.cpu().numpy(), inp.end.cpu().numpy()
+    ref_conf = gpu_confidence(gpu, inp)
+    check_defaults(*[t.cpu().numpy() for t in ref_conf], m0, start, end, range(B))
+    rows = row_source(inp.logits.cpu())
+    for rule, p in [("profile", 1.0), ("threshold", 0.9), ("robust", 0.75)]:
+        eta, eta_u, eta_o = _eta_for(rule, p, B, L, B + L)
+        mask, x, o = _decode(gpu, inp, rule, p, eta=eta, eta_uniform=eta_u)
+        r = oracle.decode_step(rows, B, L, m0, start, end, x0, rule, p, eta=eta_o)
+        compare_selection(o["commit"].cpu().numpy(), o["n_commit"].cpu().numpy(), r.commit,
+                          r.n_commit, r.flagged, range(B))
+        ok = ~r.flagged
+        assert np.array_equal(x.cpu().numpy()[ok], r.x[ok])
+        assert np.array_equal(mask.cpu().numpy()[ok], r.mask[ok])
+        for name, t in zip(("tokens", "conf", "eps", "lse"), ref_conf):
+            assert torch.equal(o[name].view(torch.int32), t.view(torch.int32)), name
