@@ -23,10 +23,10 @@
 //     greedy element enters the sum as exactly the value the final step
 //     recomputes, so s' = sum_{v != t} exp(l_v - M) is recovered by an
 //     exact subtraction and eps keeps its relative accuracy when c -> 1;
-//   * the argmax is tracked per batch (the batch in which the lane's maximum
-//     first appeared); at the end, lanes holding the row maximum re-read
-//     that batch to find the lowest index, then a wave minimum gives the
-//     lowest index of the whole row;
+//   * the argmax is tracked per batch: each lane keeps, in registers, the
+//     batch in which its maximum first appeared; at the end, lanes holding
+//     the row maximum scan that batch for the lowest index, then a wave
+//     minimum gives the lowest index of the whole row;
 //   * wavefront reductions use DPP row operations, ds_swizzle and
 //     v_readlane; partials of a split row meet in LDS in fixed order, so
 //     results do not depend on scheduling.
@@ -136,7 +136,13 @@ __device__ __forceinline__ WavePartial row_pass(const typename Vec::Raw* __restr
   double acc[kAcc];
 #pragma unroll
   for (int a = 0; a < kAcc; ++a) acc[a] = 0.0;
+  // the batch in which this lane's maximum first appeared, and its vectors:
+  // the lowest index of the row maximum is found in registers at the end
+  // (a re-read from memory would cost a dependent HBM latency per row)
   int rec = -1;
+  Raw keep[U];
+#pragma unroll
+  for (int u = 0; u < U; ++u) keep[u] = Vec::pad();
 
   auto consume = [&](const Raw (&r)[U], int batch) {
     float x[U][E];
@@ -148,6 +154,8 @@ __device__ __forceinline__ WavePartial row_pass(const typename Vec::Raw* __restr
 #pragma unroll
       for (int e = 0; e < E; ++e) bm = fmaxf(bm, x[u][e]);
     rec = bm > m ? batch : rec;
+#pragma unroll
+    for (int u = 0; u < U; ++u) keep[u] = bm > m ? r[u] : keep[u];
     const float mn = fmaxf(m, bm);
     // a lane that has only seen padding keeps a finite reference, so that
     // padding terms are exp2(-inf) = 0 rather than exp2(-inf + inf)
@@ -211,15 +219,16 @@ __device__ __forceinline__ WavePartial row_pass(const typename Vec::Raw* __restr
 
   WavePartial out;
   out.m = wave_max(m);
-  // lowest index of the maximum: lanes holding it re-read their batch
+  // lowest index of the maximum: lanes holding it scan their kept batch
   int first = 0x7fffffff;
   if (m == out.m && rec >= 0) {
+#pragma unroll
     for (int u = U - 1; u >= 0; --u) {
       const int j = rec * U + u;
       const int v = (w + j * S) * kWave + lane;
       if (j < nj && v < nvec) {
         float x[E];
-        Vec::unpack(row[v], x);
+        Vec::unpack(keep[u], x);
 #pragma unroll
         for (int e = E - 1; e >= 0; --e)
           if (x[e] == out.m) first = v * E + e;
