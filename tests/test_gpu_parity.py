@@ -227,6 +227,54 @@ def test_determinism_and_identical_rows(gpu):
         assert torch.equal(op["commit"], of["commit"]) and torch.equal(op["n_commit"], of["n_commit"])
 
 
+REPEATED_MAX = [
+    # (B, L, V, dtype): the row maximum repeats in many lanes and batches
+    (130, 3, 126464, torch.bfloat16),         # fused plan for the decode step
+    (2, 24, 40000, torch.bfloat16),           # rows split 8 ways
+    (1, 20, 70001, torch.bfloat16),           # split 16 ways, scalar path
+    (2, 9, 126464, torch.float32),
+]
+
+
+def _repeated_max_case(B, L, V, dt, seed):
+    """Integer logits in [-8, 8], so the value 8 appears about V/17 times per
+    row.  Position 0 of every sequence is a constant row (every element is a
+    maximum), position 1 has its only maximum at the last element and
+    position 2 at the first and the last."""
+    g = torch.Generator(device="cuda").manual_seed(seed)
+    logits = torch.randint(-8, 9, (B, L, V), generator=g, device="cuda").to(dt)
+    logits[:, 0, :] = 3
+    logits[:, 1:3, :] = logits[:, 1:3, :].clamp(max=7)
+    logits[:, 1, V - 1] = 8
+    logits[:, 2, 0] = 8
+    logits[:, 2, V - 1] = 8
+    mask = torch.ones((B, L), dtype=torch.uint8, device="cuda")
+    start = torch.zeros(B, dtype=torch.int32, device="cuda")
+    end = torch.full((B,), L, dtype=torch.int32, device="cuda")
+    x = torch.full((B, L), -1, dtype=torch.int32, device="cuda")
+    return workloads.StepInputs(logits, mask, start, end, x, f"repeated maxima B={B} L={L} V={V} {dt}")
+
+
+@pytest.mark.parametrize("B,L,V,dt", REPEATED_MAX)
+def test_argmax_with_repeated_maxima(gpu, B, L, V, dt):
+    """Ties broken to the lowest index when the maximum value repeats
+    thousands of times per row, across lanes, batches and split parts."""
+    inp = _repeated_max_case(B, L, V, dt, seed=B + L + V)
+    say(f"[repeated max] {inp.name}")
+    gt = gpu_confidence(gpu, inp)
+    g = [t.cpu().numpy() for t in gt]
+    first = inp.logits.float().cpu().numpy().argmax(axis=-1)   # numpy: first occurrence
+    assert np.array_equal(g[0], first)
+    assert (g[0][:, 0] == 0).all() and (g[0][:, 1] == V - 1).all() and (g[0][:, 2] == 0).all()
+    o = oracle_confidence_subset(inp, range(B))
+    mask, start, end = inp.mask.cpu().numpy(), inp.start.cpu().numpy(), inp.end.cpu().numpy()
+    worst = compare_rows(*g, *o, candidates(mask, start, end, range(B)))
+    _, _, od = _decode(gpu, inp, "profile", 1.0)
+    for name, t in zip(("tokens", "conf", "eps", "lse"), gt):
+        assert torch.equal(od[name].view(torch.int32), t.view(torch.int32)), name
+    say(f"  worst rel err {worst}")
+
+
 def _tied_profiles(B, L, seed):
     """conf on a coarse grid (many exact ties) with a few large gaps."""
     g = torch.Generator().manual_seed(seed)
