@@ -56,6 +56,9 @@
 #ifndef FDLLM_U_F32
 #define FDLLM_U_F32 4
 #endif
+#ifndef FDLLM_U_SPLIT_BF16
+#define FDLLM_U_SPLIT_BF16 2   // bf16 rows split over several waves: shorter parts, fewer registers
+#endif
 #ifndef FDLLM_TARGET_WAVES
 #define FDLLM_TARGET_WAVES 16384  // small batches: split rows until about this many waves stream
 #endif
@@ -72,6 +75,7 @@ typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 struct VecBf16x8 {
   static constexpr int kElems = 8;
   static constexpr int kU = FDLLM_U_BF16;   // vectors per lane per batch
+  static constexpr int kUSplit = FDLLM_U_SPLIT_BF16;   // the same, rows split over waves
   using Raw = u32x4;
   __device__ static Raw pad() { return Raw{0xFF80FF80u, 0xFF80FF80u, 0xFF80FF80u, 0xFF80FF80u}; }
   __device__ static void unpack(const Raw& r, float (&x)[kElems]) {
@@ -84,6 +88,7 @@ struct VecBf16x8 {
 struct VecF32x4 {
   static constexpr int kElems = 4;
   static constexpr int kU = FDLLM_U_F32;
+  static constexpr int kUSplit = FDLLM_U_F32;
   using Raw = u32x4;
   __device__ static Raw pad() { return Raw{0xFF800000u, 0xFF800000u, 0xFF800000u, 0xFF800000u}; }
   __device__ static void unpack(const Raw& r, float (&x)[kElems]) {
@@ -94,6 +99,7 @@ struct VecF32x4 {
 struct VecBf16x1 {
   static constexpr int kElems = 1;
   static constexpr int kU = 8;
+  static constexpr int kUSplit = 8;
   using Raw = unsigned short;
   __device__ static Raw pad() { return (unsigned short)0xFF80u; }
   __device__ static void unpack(const Raw& r, float (&x)[kElems]) { x[0] = __uint_as_float((unsigned)r << 16); }
@@ -101,6 +107,7 @@ struct VecBf16x1 {
 struct VecF32x1 {
   static constexpr int kElems = 1;
   static constexpr int kU = 8;
+  static constexpr int kUSplit = 8;
   using Raw = unsigned int;
   __device__ static Raw pad() { return 0xFF800000u; }
   __device__ static void unpack(const Raw& r, float (&x)[kElems]) { x[0] = __uint_as_float(r); }
@@ -927,7 +934,8 @@ static hipError_t launch_confidence_t(const void* logits, int B, int L, int nvec
   case SPLIT: {                                                                                 \
     using Sh = SplitShape<SPLIT>;                                                               \
     const long long grid = (nvslots + Sh::kRows - 1) / Sh::kRows;                               \
-    hipLaunchKernelGGL((k_confidence<Vec, Vec::kU, SPLIT>), dim3((unsigned)grid), dim3(Sh::kThreads), \
+    hipLaunchKernelGGL((k_confidence<Vec, SPLIT == 1 ? Vec::kU : Vec::kUSplit, SPLIT>),           \
+                       dim3((unsigned)grid), dim3(Sh::kThreads),                                \
                        0, st, lg, B, L, nvec, mask, bs, be, out);                               \
     break;                                                                                      \
   }
@@ -953,10 +961,10 @@ static hipError_t launch_confidence_parts_t(const void* logits, int B, int L, in
   const auto* lg = (const typename Vec::Raw*)logits;
   const dim3 grid((unsigned)(nslots * (split / 4))), block(256);
   if (split == 8)
-    hipLaunchKernelGGL((k_confidence_parts<Vec, Vec::kU, 8>), grid, block, 0, st, lg, B, L, nvec,
+    hipLaunchKernelGGL((k_confidence_parts<Vec, Vec::kUSplit, 8>), grid, block, 0, st, lg, B, L, nvec,
                        mask, bs, be, out, parts);
   else if (split == 16)
-    hipLaunchKernelGGL((k_confidence_parts<Vec, Vec::kU, 16>), grid, block, 0, st, lg, B, L, nvec,
+    hipLaunchKernelGGL((k_confidence_parts<Vec, Vec::kUSplit, 16>), grid, block, 0, st, lg, B, L, nvec,
                        mask, bs, be, out, parts);
   else
     return hipErrorInvalidValue;
