@@ -195,8 +195,9 @@ def _candidates(inp) -> int:
     return int((inwin & inp.mask.bool()).sum())
 
 
-def _time_steps(fd, torch, inp, selector, p, reps, scratch=None):
-    """Average decode-step kernel time (HIP events) over reps, input state restored."""
+def _time_steps(fd, torch, inp, selector, p, reps, scratch=None, settle=None):
+    """Average decode-step kernel time (HIP events) over reps, input state restored;
+    `settle` (if given) brings the clocks to their loaded state first."""
     B = inp.logits.shape[0]
     mask0, x0 = inp.mask.clone(), inp.x.clone()
     mask, x = mask0.clone(), x0.clone()
@@ -204,6 +205,8 @@ def _time_steps(fd, torch, inp, selector, p, reps, scratch=None):
     ws = fd.fdllm_decode_step(inp.logits, mask, inp.start, inp.end, x, selector, p, n_commit=nc)
     evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
            for _ in range(reps)]
+    if settle is not None:
+        settle()
     for k in range(reps):
         mask.copy_(mask0)
         x.copy_(x0)
@@ -230,7 +233,7 @@ def _row(name, shape, sel, positions, bytes_, t_cold, t_hot, stream_gbps, extra=
     return d
 
 
-def per_workload_report(fd, torch, workloads, dev, stream_gbps, reps):
+def per_workload_report(fd, torch, workloads, dev, stream_gbps, reps, settle=None):
     import gc
     rows = []
     scratch = torch.empty(512 << 20, dtype=torch.uint8, device=dev)
@@ -243,8 +246,9 @@ def per_workload_report(fd, torch, workloads, dev, stream_gbps, reps):
         pos = _candidates(inp)
         nbytes = pos * V * inp.logits.element_size()
         for sel, p in sels[k]:
-            tc, _, commits = _time_steps(fd, torch, inp, sel, p, reps, scratch if cold_needed else None)
-            th = _time_steps(fd, torch, inp, sel, p, reps)[0] if cold_needed else None
+            tc, _, commits = _time_steps(fd, torch, inp, sel, p, reps, scratch if cold_needed else None,
+                                         settle)
+            th = _time_steps(fd, torch, inp, sel, p, reps, settle=settle)[0] if cold_needed else None
             extra = {"mean_commits_per_block": commits}
             if not cold_needed:
                 extra["note"] = "cold by size: the step reads far more than the caches hold"
@@ -332,6 +336,8 @@ def per_workload_report(fd, torch, workloads, dev, stream_gbps, reps):
         # stays full and host launch gaps stay out of the per-call times
         burst = 4
         tf, tg, tp = [], [], []
+        if settle is not None:
+            settle()
         for _ in range(max(3, reps // 2)):
             e0, e1, e2, e3 = (torch.cuda.Event(enable_timing=True) for _ in range(4))
             e0.record()
@@ -666,7 +672,7 @@ def main():
         "source_sha256_16": source_digest(),
     }
     if args.per_workload:
-        rows = per_workload_report(fd, torch, workloads, dev, stream_gbps, reps=10)
+        rows = per_workload_report(fd, torch, workloads, dev, stream_gbps, reps=10, settle=settle)
         line["per_workload"] = rows + stress_rows
         if args.per_workload_md:
             cmd = "python bench.py " + " ".join(sys.argv[1:])
