@@ -207,6 +207,11 @@ def _time_steps(fd, torch, inp, selector, p, reps, scratch=None, settle=None):
            for _ in range(reps)]
     if settle is not None:
         settle()
+    for _ in range(2):                       # warm-up on this workload's own buffers
+        mask.copy_(mask0)
+        x.copy_(x0)
+        fd.fdllm_decode_step(inp.logits, mask, inp.start, inp.end, x, selector, p, n_commit=nc,
+                             workspace=ws)
     for k in range(reps):
         mask.copy_(mask0)
         x.copy_(x0)
