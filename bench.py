@@ -17,9 +17,10 @@ Prints one JSON line.  `value` is masked positions per second over the whole
 timed region; `roofline` relates the fused kernel's algorithmic bytes to its
 average launch time measured with HIP events on the launch stream, and to a
 read-only stream of the same logits buffer (libfdllm_bench.so).
-`cpu_baseline` times the CPU oracle on a bounded sample of the same workload:
-on all host cores (one process per core, each on its own sequences) and on
-one core.  `--per-workload` adds the other workload recipes (one sequence fp32;
+`parity` compares the outputs of the timed step with the CPU oracle run on
+exact host copies of every one of its logits rows, and `cpu_baseline` times
+that oracle run (all host cores, one worker process per core) and a one-core
+run on a seeded sample of its blocks.  `--per-workload` adds the other workload recipes (one sequence fp32;
 eight-sequence and 256-sequence simulated generations; 64 sequences in a
 512-position span), cold and cache-hot, the device-resident generation loop
 and the LM head fused with the pass, and can write them as a markdown table.
@@ -88,80 +89,69 @@ def under_profiler() -> bool:
 
 
 # ---------------------------------------------------------------------------
-# CPU oracle on all host cores: one spawned process per core, CPU only.  The
-# processes start before this process touches the GPU, build their own
-# sequences of the same recipe on the CPU, report ready, and run the oracle
-# when released; the parallel time is last finish minus first start.
+# CPU oracle: parity of the timed step and the CPU baseline.  The worker
+# processes (oracle.parallel) are spawned before this process touches the GPU;
+# after the GPU timing they run the oracle on exact host copies of the timed
+# step's logits rows and the outputs of its last run are compared with it.
 # ---------------------------------------------------------------------------
-def _oracle_worker(blocks, rule, param, ready, go, results):
+def oracle_parity(pool, inp, saved, rule: str, param: float):
+    """Oracle on every candidate row of the timed step (all host cores), and
+    the comparison with the saved GPU outputs of that step."""
     import numpy as np
     import torch
-    torch.set_num_threads(1)
-    import oracle
-    import workloads
-    rows = torch.stack([workloads.stress_b1024_l32_rows(b, "cpu") for b in blocks])     # [n, L, V] bf16
-    n, L, _ = rows.shape
-    mask = np.ones((n, L), dtype=np.uint8)
-    start = np.zeros(n, dtype=np.int64)
-    end = np.full(n, L, dtype=np.int64)
-    x = np.full((n, L), -1, dtype=np.int64)
-    get = lambda b, i: rows[b, i].to(torch.float64).numpy()
-    ready.put(os.getpid())
-    go.wait()
-    t0 = time.time()
-    r = oracle.decode_step(get, n, L, mask, start, end, x, rule, param)
-    t1 = time.time()
-    results.put((t0, t1, int(mask.sum()), int(r.n_commit.sum())))
+    from oracle.parallel import scatter_confidence
+    B, L, V = inp.logits.shape
+    mask = inp.mask0.cpu().numpy()
+    start, end = inp.start.cpu().numpy(), inp.end.cpu().numpy()
+    cells = [(b, i) for b in range(B) for i in range(int(start[b]), int(end[b])) if mask[b, i]]
+    flat = inp.logits.view(B * L, V)
+    idx = torch.tensor([b * L + i for b, i in cells], dtype=torch.long, device=inp.logits.device)
+
+    def fill(first, cnt, out):
+        rows = flat.index_select(0, idx[first:first + cnt])
+        torch.from_numpy(out).copy_(rows.view(torch.int16))
+
+    s0 = pool.seconds
+    res = pool.rows_confidence(fill, len(cells), V, "bf16")
+    tok, conf, eps, lse = scatter_confidence(B, L, cells, res)
+    commit, n_commit, flagged = pool.select(eps, conf, mask, start, end, rule, param)
+    secs = pool.seconds - s0
+    g = {k: v.cpu().numpy() for k, v in saved.items()}
+    ci = tuple(np.array(c) for c in zip(*cells))
+    rel = lambda a, b, floor: np.abs(a[ci].astype(np.float64) - b[ci]) / np.maximum(np.abs(b[ci]), floor)
+    e_conf, e_lse = rel(g["conf"], conf, 1e-30), rel(g["lse"], lse, 1.0)
+    d_eps = np.abs(g["eps"][ci].astype(np.float64) - eps[ci])
+    e_eps = np.where(d_eps > 2.0 ** -48, d_eps / np.maximum(np.abs(eps[ci]), 1e-30), 0.0)
+    same = np.array([np.array_equal(g["commit"][b], commit[b]) and int(g["n_commit"][b]) == int(n_commit[b])
+                     for b in range(B)])
+    hit = commit.astype(bool)
+    ox, om = inp.x0.cpu().numpy().copy(), mask.copy()
+    ox[hit] = tok[hit]
+    om[hit] = 0
+    same_seq = np.array([np.array_equal(g["x"][b], ox[b]) and np.array_equal(g["mask"][b], om[b])
+                         for b in range(B)])
+    parity = {"rule": f"{rule}({param})", "checked_blocks": B, "checked_positions": len(cells),
+              "token_mismatches": int((g["tokens"][ci] != tok[ci]).sum()),
+              "value_mismatches": int(((e_conf > 1e-5) | (e_eps > 1e-5) | (e_lse > 1e-5)).sum()),
+              "mismatches": int((~same & ~flagged).sum() + (~same_seq & ~flagged).sum()),
+              "flagged": int(flagged.sum()), "flagged_matching": int((same & flagged).sum()),
+              "max_rel_err": {"conf": float(e_conf.max()), "eps": float(e_eps.max()),
+                              "lse": float(e_lse.max())},
+              "oracle": "oracle.position_confidence (float64, fsum) + oracle.select (exact rationals) "
+                        "on device-to-host copies of the timed step's rows"}
+    base = {"value": len(cells) / secs, "unit": "masked positions/s", "cores": pool.workers,
+            "kind": "oracle",
+            "sample": f"the whole timed step: {B} blocks, {len(cells)} positions "
+                      f"({len(cells) * V * 2 / 1e9:.2f} GB of bf16 logits copied device-to-host), "
+                      f"{rule} f={param}; {pool.workers} processes, NumPy float64 + exact rational "
+                      f"selection; {secs:.1f} s inside the oracle calls (staging copies excluded)",
+            "seconds": secs, "logits_GBps": len(cells) * V * 2 / secs / 1e9}
+    return parity, base
 
 
-class OracleCrew:
-    def __init__(self, n_workers: int, blocks_per_worker: int, rule: str, param: float):
-        ctx = mp.get_context("spawn")
-        self.ready, self.results, self.go = ctx.Queue(), ctx.Queue(), ctx.Event()
-        self.bpw = blocks_per_worker
-        self.procs = [ctx.Process(target=_oracle_worker,
-                                  args=(list(range(w * blocks_per_worker, (w + 1) * blocks_per_worker)),
-                                        rule, param, self.ready, self.go, self.results), daemon=True)
-                      for w in range(n_workers)]
-        for p in self.procs:
-            p.start()
-
-    def _collect(self, q, timeout: float):
-        """One item per process from q; raises if a process died or time ran out."""
-        import queue
-        items, deadline = [], time.time() + timeout
-        while len(items) < len(self.procs):
-            try:
-                items.append(q.get(timeout=1.0))
-            except queue.Empty:
-                dead = [p.exitcode for p in self.procs if p.exitcode not in (None, 0)]
-                if dead:
-                    raise RuntimeError(f"oracle process exited with status {dead[0]}")
-                if time.time() > deadline:
-                    raise TimeoutError("oracle processes did not finish in time")
-        return items
-
-    def wait_ready(self, timeout: float):
-        self._collect(self.ready, timeout)
-
-    def run(self, timeout: float):
-        self.go.set()
-        res = self._collect(self.results, timeout)
-        for p in self.procs:
-            p.join(timeout=30)
-        t0 = min(r[0] for r in res)
-        t1 = max(r[1] for r in res)
-        return t1 - t0, sum(r[2] for r in res), sum(r[3] for r in res), max(r[1] - r[0] for r in res)
-
-    def stop(self):
-        for p in self.procs:
-            if p.is_alive():
-                p.terminate()
-                p.join(timeout=10)
-
-
-def cpu_baseline_single(inp, n_blocks: int, rule: str, param: float):
-    """The oracle on one core, on a seeded sample of blocks of the timed step."""
+def cpu_baseline_single(inp, saved, n_blocks: int, rule: str, param: float):
+    """The oracle in this process (one core) on a seeded sample of blocks of the
+    timed step, checked against the saved GPU outputs of those blocks."""
     import numpy as np
     import torch
     import oracle
@@ -169,19 +159,23 @@ def cpu_baseline_single(inp, n_blocks: int, rule: str, param: float):
     rng = np.random.default_rng(7)
     blocks = sorted(rng.choice(B, n_blocks, replace=False).tolist())
     rows = inp.logits[blocks].to("cpu")                      # [n, L, V] bf16, outside the timing
-    mask = inp.mask[blocks].cpu().numpy()
+    mask = inp.mask0[blocks].cpu().numpy()
     start, end = inp.start[blocks].cpu().numpy(), inp.end[blocks].cpu().numpy()
-    x = inp.x[blocks].cpu().numpy()
+    x = inp.x0[blocks].cpu().numpy()
     get = lambda b, i: rows[b, i].to(dtype=torch.float64).numpy()
     t0 = time.perf_counter()
     r = oracle.decode_step(get, n_blocks, L, mask, start, end, x, rule, param)
     dt = time.perf_counter() - t0
     n_pos = int(mask.sum())
+    gc_, gn = saved["commit"][blocks].cpu().numpy(), saved["n_commit"][blocks].cpu().numpy()
+    same = np.array([np.array_equal(gc_[k], r.commit[k]) and int(gn[k]) == int(r.n_commit[k])
+                     for k in range(n_blocks)])
     return {"value": n_pos / dt, "unit": "masked positions/s", "cores": 1, "kind": "oracle",
             "sample": f"{n_blocks} of {B} blocks ({n_pos} positions, {n_pos * V * 2 / 1e9:.2f} GB of "
                       f"bf16 logits) of the timed step, {rule} f={param}; one process, NumPy float64 "
                       f"+ exact rational selection; {dt:.1f} s",
-            "seconds": dt, "logits_GBps": n_pos * V * 2 / dt / 1e9, "commits": int(r.n_commit.sum())}
+            "seconds": dt, "logits_GBps": n_pos * V * 2 / dt / 1e9, "commits": int(r.n_commit.sum()),
+            "blocks_matching_gpu": int(same.sum()), "blocks_flagged": int(r.flagged.sum())}
 
 
 # ---------------------------------------------------------------------------
@@ -485,7 +479,6 @@ def main():
     ap.add_argument("--cpu-blocks", type=int, default=90, help="blocks in the one-core oracle sample")
     ap.add_argument("--cpu-workers", type=int, default=0,
                     help="processes of the all-core oracle run (0: host CPUs, at most 16)")
-    ap.add_argument("--cpu-worker-blocks", type=int, default=60, help="blocks per oracle process")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-selector-sweep", action="store_true")
     ap.add_argument("--per-workload", action="store_true", help="also time the other workload recipes")
@@ -509,17 +502,19 @@ def main():
         lmhead_only(args.lmhead_positions, args.steps, args.warmup)
         return
 
-    crew, crew_note = None, None
+    pool, pool_note = None, None
     if not args.no_cpu_baseline:
         if under_profiler():
-            crew_note = "all-core oracle run skipped under a profiler"
+            # the profiler's preloaded library has initialised the GPU already,
+            # and processes are not spawned from such a process
+            pool_note = "oracle run (parity and all-core baseline) skipped under a profiler"
         else:
-            n_w = args.cpu_workers or min(MAX_HOST_WORKERS, len(os.sched_getaffinity(0)))
             try:
-                crew = OracleCrew(n_w, args.cpu_worker_blocks, args.selector, param)
-                log(f"cpu_baseline: started {n_w} oracle processes")
+                from oracle.parallel import OraclePool
+                pool = OraclePool(args.cpu_workers or min(MAX_HOST_WORKERS, len(os.sched_getaffinity(0))))
+                log(f"cpu_baseline: started {pool.workers} oracle processes")
             except Exception as e:          # no process support: one-core figure only
-                crew_note = f"all-core oracle run unavailable: {e!r}"
+                pool_note = f"all-core oracle run unavailable: {e!r}"
 
     import torch
     import paper_2606_02955_amd as fd
@@ -542,13 +537,6 @@ def main():
                 commit=torch.empty((B, L), dtype=torch.uint8, device=dev),
                 n_commit=torch.empty((B,), dtype=torch.int32, device=dev))
     torch.cuda.synchronize()
-
-    if crew is not None:
-        try:
-            crew.wait_ready(timeout=600)    # no host load from the crew during GPU timing
-        except Exception as e:
-            crew.stop()
-            crew, crew_note = None, f"all-core oracle run unavailable: {e!r}"
 
     copy_ref = None
     if args.copy_calibration_mb > 0:
@@ -622,6 +610,10 @@ def main():
 
     wall, kavg, kmin = run(args.selector, param, args.steps, args.warmup, f"{args.selector}({param})")
     commits = float(outs["n_commit"].float().mean())
+    # the headline run's outputs (every timed step computes the same), kept for the parity check
+    saved = {k: v.clone() for k, v in outs.items()}
+    saved.update(mask=mask.clone(), x=x.clone())
+    inp.mask0, inp.x0 = mask0, x0
     sweep = {}
     stress_rows = [_row(workloads.RECIPE_NAMES[workloads.STRESS], "B=1024 L=32 V=126464 bf16", f"{args.selector}({param})", positions,
                     logits_bytes, kavg, None, stream_gbps, {"mean_commits_per_block": commits})]
@@ -684,29 +676,27 @@ def main():
             with open(args.per_workload_md, "w") as fh:
                 fh.write(per_workload_markdown(rows, stress_rows, stream_gbps, cmd))
     if not args.no_cpu_baseline:
-        log(f"cpu_baseline: oracle on {args.cpu_blocks} blocks, one core")
-        single = cpu_baseline_single(inp, args.cpu_blocks, args.selector, param)
-        single["cpu_model"] = cpu_model()
-        base = dict(single)
-        if crew is not None:
-            log(f"cpu_baseline: oracle on {len(crew.procs)} processes")
+        base = None
+        if pool is not None:
+            log(f"parity: oracle on every block of the timed step, {pool.workers} processes")
             try:
-                wall_c, pos_c, commits_c, slowest = crew.run(timeout=900)
-                base = {"value": pos_c / wall_c, "unit": "masked positions/s",
-                        "cores": len(crew.procs), "kind": "oracle",
-                        "sample": f"{len(crew.procs)} processes x {crew.bpw} sequences of the same "
-                                  f"recipe built on the CPU ({pos_c} positions, "
-                                  f"{pos_c * V * 2 / 1e9:.2f} GB of bf16 logits), {args.selector} "
-                                  f"f={param}; NumPy float64 + exact rational selection; "
-                                  f"{wall_c:.1f} s from first start to last finish",
-                        "seconds": wall_c, "logits_GBps": pos_c * V * 2 / wall_c / 1e9,
-                        "commits": commits_c, "cpu_model": cpu_model(), "single_core": single}
+                parity, base = oracle_parity(pool, inp, saved, args.selector, param)
+                line["parity"] = parity
+                log(f"parity: {parity['mismatches']} mismatches, {parity['flagged']} flagged, "
+                    f"{parity['token_mismatches']} token / {parity['value_mismatches']} value mismatches")
             except Exception as e:
-                base["note"] = f"all-core oracle run failed: {e!r}"
+                pool_note = f"all-core oracle run failed: {e!r}"
             finally:
-                crew.stop()
-        elif crew_note:
-            base["note"] = crew_note
+                pool.close()
+        log(f"cpu_baseline: oracle on {args.cpu_blocks} blocks, one core")
+        single = cpu_baseline_single(inp, saved, args.cpu_blocks, args.selector, param)
+        single["cpu_model"] = cpu_model()
+        if base is None:
+            base = dict(single)
+            if pool_note:
+                base["note"] = pool_note
+        else:
+            base.update(cpu_model=cpu_model(), single_core=single)
         base["host_cpus_available"] = len(os.sched_getaffinity(0))
         line["cpu_baseline"] = base
     else:

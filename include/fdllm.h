@@ -34,8 +34,14 @@
  *   (FDLLM_MAX_BLOCK).  Blocks of up to 64 positions are selected within one
  *   64-lane wavefront, larger ones (block-size ablations) by a workgroup.
  *   Bounds live in device memory and are checked on the device: a sequence
- *   with invalid bounds gets no commits, default outputs and n_commit = -1.
- * Logits.  Must be finite with |logit| < 1e30 (NaN/inf are not supported).
+ *   with invalid bounds gets no commits, default outputs and n_commit = -1
+ *   (where n_commit is written).  fdllm_check_inputs reports such sequences
+ *   to the host.
+ * Logits.  Must be finite with |logit| <= FDLLM_MAX_ABS_LOGIT (1e7).  Within
+ *   that range every row's exponent reference is exact (the row maximum's own
+ *   term lies in (1/2, 1]), so results do not depend on the logits' offset.
+ *   NaN, inf and larger magnitudes are outside the contract (results are
+ *   unspecified, no fault); fdllm_check_inputs detects them.
  * Ties.  The argmax takes the lowest vocabulary index; the confidence sort
  *   puts equal values at the lower position first.
  * Streams.  Every call only enqueues work on `stream` (NULL = the null
@@ -77,8 +83,13 @@ typedef int fdllm_status;
 #define FDLLM_ERR_SIZE (-3)              /* V < 1, or B*L*V beyond 2^62 elements     */
 #define FDLLM_ERR_WORKSPACE (-4)         /* workspace missing or too small           */
 #define FDLLM_ERR_HIP (-5)               /* the HIP runtime rejected a launch        */
+#define FDLLM_ERR_BOUNDS (-6)            /* fdllm_check_inputs: a window outside [0, L] */
+#define FDLLM_ERR_BLOCK_TOO_LARGE (-7)   /* fdllm_check_inputs: end - start > FDLLM_MAX_BLOCK */
+#define FDLLM_ERR_NONFINITE (-8)         /* fdllm_check_inputs: a candidate logit is NaN,
+                                            inf or beyond FDLLM_MAX_ABS_LOGIT           */
 
 #define FDLLM_MAX_BLOCK 1024
+#define FDLLM_MAX_ABS_LOGIT 1.0e7f
 
 /*
  * Greedy token, confidence, complement and log-sum-exp of every candidate
@@ -324,6 +335,25 @@ fdllm_status fdllm_generation_create(const fdllm_generation_desc* desc, fdllm_ge
 fdllm_status fdllm_generation_run(fdllm_generation gen, fdllm_stream stream, int32_t* steps);
 
 fdllm_status fdllm_generation_destroy(fdllm_generation gen);
+
+/*
+ * Opt-in input check (debug aid; the other entry points never read the
+ * logits of non-candidates and do not validate values).  Scans every
+ * candidate row (as defined above) for a logit that is NaN, inf or of
+ * magnitude above FDLLM_MAX_ABS_LOGIT, and every sequence's window.
+ *   logits, dtype, B, L, V, mask, block_start, block_end: as fdllm_confidence;
+ *   counts [3] int32 device memory (out): sequences whose window is not
+ *   0 <= start <= end <= L; sequences whose window is longer than
+ *   FDLLM_MAX_BLOCK; candidate rows holding a bad logit (rows of sequences
+ *   with an invalid window are not scanned).
+ * Unlike the other entry points this call SYNCHRONISES `stream` and returns
+ * the verdict: FDLLM_ERR_BOUNDS, else FDLLM_ERR_BLOCK_TOO_LARGE, else
+ * FDLLM_ERR_NONFINITE when the matching count is non-zero, else FDLLM_OK.
+ * It reads every candidate logit once (the same traffic as the pass).
+ */
+fdllm_status fdllm_check_inputs(const void* logits, fdllm_dtype dtype, int B, int L, int V,
+                                const uint8_t* mask, const int32_t* block_start,
+                                const int32_t* block_end, int32_t* counts, fdllm_stream stream);
 
 /* Workspace bytes fdllm_decode_step needs for these sizes (0 = none). */
 fdllm_status fdllm_workspace_size(int B, int L, int V, fdllm_dtype dtype, size_t* bytes);

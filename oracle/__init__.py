@@ -11,7 +11,8 @@ CPU restatement of what one decoding step of the paper's method computes:
     variant (appendix "Calibration-Robust Frechet Certificates"), by
     Fast-dLLM's factor rule and by the threshold rule (Sec. 2,
     "Confidence-Aware Parallel Decoding"; Sec. 5, "Baselines");
-  * the reveal of the chosen tokens (Alg. 1, reveal step);
+  * the reveal of the chosen tokens (Alg. 1, reveal step), and the move of
+    a finished block's window to the next block (Alg. 1, outer loop);
   * for the LM-head form, the logits as float64 dot products of hidden
     states with the output embedding (``lmhead``).
 
@@ -34,11 +35,12 @@ from .rules import (sorted_order, factor_n_star, profile_n_star, profile_literal
                      profile_adaptive_n_star, threshold_set, select_block, select, SelectResult,
                      frechet_quantities, robust_eps, FLAG_WINDOW)
 from .step import decode_step, StepResult
+from .loop import advance_blocks
 from . import lmhead
 
 __all__ = [
     "position_confidence", "confidence", "sorted_order", "factor_n_star", "profile_n_star",
     "profile_literal_n_star", "profile_adaptive_n_star", "threshold_set", "select_block",
     "select", "SelectResult", "frechet_quantities", "robust_eps", "FLAG_WINDOW", "decode_step", "StepResult",
-    "lmhead",
+    "advance_blocks", "lmhead",
 ]

@@ -26,13 +26,15 @@ MAX_BLOCK = 1024
 
 OK = 0
 ERR_INVALID_ARG, ERR_UNSUPPORTED_DTYPE, ERR_SIZE, ERR_WORKSPACE, ERR_HIP = -1, -2, -3, -4, -5
+ERR_BOUNDS, ERR_BLOCK_TOO_LARGE, ERR_NONFINITE = -6, -7, -8
+MAX_ABS_LOGIT = 1.0e7
 
 EXPORTS = ("fdllm_confidence", "fdllm_select_profile", "fdllm_select_factor",
            "fdllm_select_threshold", "fdllm_select_robust", "fdllm_reveal", "fdllm_decode_step",
            "fdllm_workspace_size", "fdllm_status_string", "fdllm_synth_logits",
            "fdllm_advance_blocks", "fdllm_generation_workspace_size", "fdllm_generation_create",
            "fdllm_generation_run", "fdllm_generation_destroy", "fdllm_lmhead_workspace_size",
-           "fdllm_lmhead_confidence", "fdllm_lmhead_decode_step")
+           "fdllm_lmhead_confidence", "fdllm_lmhead_decode_step", "fdllm_check_inputs")
 
 
 class GenerationDesc(ctypes.Structure):
@@ -78,6 +80,7 @@ def load(path: Optional[str] = None) -> ctypes.CDLL:
     lib.fdllm_reveal.argtypes = [vp, vp, vp, vp, i32, i32, vp]
     lib.fdllm_decode_step.argtypes = [vp, i32, i32, i32, i32, vp, vp, vp, vp, i32, f32, vp, f32,
                                       vp, vp, vp, vp, vp, vp, vp, sz, vp]
+    lib.fdllm_check_inputs.argtypes = [vp, i32, i32, i32, i32, vp, vp, vp, vp, vp]
     lib.fdllm_workspace_size.argtypes = [i32, i32, i32, i32, ctypes.POINTER(sz)]
     lib.fdllm_status_string.argtypes = [i32]
     lib.fdllm_status_string.restype = ctypes.c_char_p
@@ -94,6 +97,7 @@ def load(path: Optional[str] = None) -> ctypes.CDLL:
     lib.fdllm_generation_run.argtypes = [vp, vp, ctypes.POINTER(i32)]
     lib.fdllm_generation_destroy.argtypes = [vp]
     for name in ("fdllm_confidence", "fdllm_reveal", "fdllm_decode_step", "fdllm_workspace_size",
+                 "fdllm_check_inputs",
                  "fdllm_synth_logits", "fdllm_advance_blocks", "fdllm_generation_workspace_size",
                  "fdllm_lmhead_workspace_size", "fdllm_lmhead_confidence", "fdllm_lmhead_decode_step",
                  "fdllm_generation_create", "fdllm_generation_run", "fdllm_generation_destroy"):
@@ -230,6 +234,23 @@ def fdllm_decode_step(logits, mask, block_start, block_end, x, selector: str, pa
         ws_ptr, ws_bytes, _stream(logits.device))
     _check(st, "fdllm_decode_step")
     return workspace
+
+
+def fdllm_check_inputs(logits, mask, block_start, block_end, counts=None):
+    """Opt-in input check (synchronises the stream).  Returns (status, counts
+    [3]: windows outside the span, windows longer than the block limit,
+    candidate rows with a NaN / inf / out-of-range logit)."""
+    B, L, V = logits.shape
+    if counts is None:
+        counts = torch.empty(3, dtype=torch.int32, device=logits.device)
+    st = load().fdllm_check_inputs(
+        _ptr(logits, name="logits"), _dtype_code(logits), B, L, V,
+        _ptr(mask, torch.uint8, (B, L), "mask"), _ptr(block_start, torch.int32, (B,), "block_start"),
+        _ptr(block_end, torch.int32, (B,), "block_end"), _ptr(counts, torch.int32, (3,), "counts"),
+        _stream(logits.device))
+    if st not in (OK, ERR_BOUNDS, ERR_BLOCK_TOO_LARGE, ERR_NONFINITE):
+        _check(st, "fdllm_check_inputs")
+    return st, [int(v) for v in counts.cpu()]
 
 
 def fdllm_lmhead_workspace_size(B: int, L: int, d: int, V: int) -> int:

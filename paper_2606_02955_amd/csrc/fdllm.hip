@@ -72,6 +72,12 @@ namespace fdllm {
 // ---------------------------------------------------------------------------
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 
+// bit pattern of FDLLM_MAX_ABS_LOGIT as a float; for finite and non-finite
+// values alike, |x| > bound  <=>  (bits(x) & 0x7FFFFFFF) > kBoundBits
+constexpr unsigned kBoundBits = 0x4B189680u;   // 1.0e7f
+static_assert(__builtin_bit_cast(unsigned, FDLLM_MAX_ABS_LOGIT) == kBoundBits, "logit bound bits");
+__device__ __forceinline__ bool bad_bits(unsigned f32bits) { return (f32bits & 0x7FFFFFFFu) > kBoundBits; }
+
 struct VecBf16x8 {
   static constexpr int kElems = 8;
   static constexpr int kU = FDLLM_U_BF16;   // vectors per lane per batch
@@ -84,6 +90,11 @@ struct VecBf16x8 {
     x[4] = __uint_as_float(r.z << 16); x[5] = __uint_as_float(r.z & 0xFFFF0000u);
     x[6] = __uint_as_float(r.w << 16); x[7] = __uint_as_float(r.w & 0xFFFF0000u);
   }
+  __device__ static bool bad(const Raw& r) {
+    return bad_bits(r.x << 16) | bad_bits(r.x & 0xFFFF0000u) | bad_bits(r.y << 16) |
+           bad_bits(r.y & 0xFFFF0000u) | bad_bits(r.z << 16) | bad_bits(r.z & 0xFFFF0000u) |
+           bad_bits(r.w << 16) | bad_bits(r.w & 0xFFFF0000u);
+  }
 };
 struct VecF32x4 {
   static constexpr int kElems = 4;
@@ -95,6 +106,9 @@ struct VecF32x4 {
     x[0] = __uint_as_float(r.x); x[1] = __uint_as_float(r.y);
     x[2] = __uint_as_float(r.z); x[3] = __uint_as_float(r.w);
   }
+  __device__ static bool bad(const Raw& r) {
+    return bad_bits(r.x) | bad_bits(r.y) | bad_bits(r.z) | bad_bits(r.w);
+  }
 };
 struct VecBf16x1 {
   static constexpr int kElems = 1;
@@ -103,6 +117,7 @@ struct VecBf16x1 {
   using Raw = unsigned short;
   __device__ static Raw pad() { return (unsigned short)0xFF80u; }
   __device__ static void unpack(const Raw& r, float (&x)[kElems]) { x[0] = __uint_as_float((unsigned)r << 16); }
+  __device__ static bool bad(const Raw& r) { return bad_bits((unsigned)r << 16); }
 };
 struct VecF32x1 {
   static constexpr int kElems = 1;
@@ -111,6 +126,7 @@ struct VecF32x1 {
   using Raw = unsigned int;
   __device__ static Raw pad() { return 0xFF800000u; }
   __device__ static void unpack(const Raw& r, float (&x)[kElems]) { x[0] = __uint_as_float(r); }
+  __device__ static bool bad(const Raw& r) { return bad_bits(r); }
 };
 
 template <class Raw>
@@ -889,6 +905,41 @@ __global__ void __launch_bounds__(256) k_reveal(const uint8_t* __restrict__ comm
 }
 
 // ---------------------------------------------------------------------------
+// opt-in input check: windows, and candidate rows holding a logit that is
+// NaN, inf or beyond FDLLM_MAX_ABS_LOGIT.  counts: [out of span, too long,
+// bad rows]; one wave per slot of the span, four per workgroup.
+// ---------------------------------------------------------------------------
+__global__ void k_check_clear(int32_t* __restrict__ counts) {
+  if (threadIdx.x < 3) counts[threadIdx.x] = 0;
+}
+
+template <class Vec>
+__global__ void __launch_bounds__(256) k_check(const typename Vec::Raw* __restrict__ logits, int B,
+                                               int L, int nvec, const uint8_t* __restrict__ mask,
+                                               const int32_t* __restrict__ bstart,
+                                               const int32_t* __restrict__ bend,
+                                               int32_t* __restrict__ counts) {
+  const int lane = threadIdx.x % kWave;
+  const long long slot = (long long)blockIdx.x * 4 + threadIdx.x / kWave;
+  if (slot >= (long long)B * L) return;
+  const int b = (int)(slot / L), i = (int)(slot % L);
+  const int s = bstart[b], e = bend[b];
+  if (!(s >= 0 && s <= e && e <= L)) {
+    if (i == 0 && lane == 0) atomicAdd(&counts[0], 1);
+    return;
+  }
+  if (e - s > kMaxBlock) {
+    if (i == 0 && lane == 0) atomicAdd(&counts[1], 1);
+    return;
+  }
+  if (i < s || i >= e || mask[slot] == 0) return;
+  const typename Vec::Raw* row = logits + slot * (long long)nvec;
+  bool bad = false;
+  for (int v = lane; v < nvec; v += kWave) bad |= Vec::bad(load_stream(row + v));
+  if (__ballot(bad) != 0ull && lane == 0) atomicAdd(&counts[2], 1);
+}
+
+// ---------------------------------------------------------------------------
 // host side: planning and launches
 // ---------------------------------------------------------------------------
 struct Plan {
@@ -1122,8 +1173,49 @@ const char* fdllm_status_string(fdllm_status st) {
     case FDLLM_ERR_SIZE: return "unsupported size (V < 1 or too many elements)";
     case FDLLM_ERR_WORKSPACE: return "workspace missing or too small";
     case FDLLM_ERR_HIP: return "HIP runtime error at launch";
+    case FDLLM_ERR_BOUNDS: return "a block window lies outside [0, L] (start > end, start < 0 or end > L)";
+    case FDLLM_ERR_BLOCK_TOO_LARGE: return "a block window is longer than FDLLM_MAX_BLOCK positions";
+    case FDLLM_ERR_NONFINITE: return "a candidate logit is NaN, inf or beyond FDLLM_MAX_ABS_LOGIT";
     default: return "unknown status";
   }
+}
+
+fdllm_status fdllm_check_inputs(const void* logits, fdllm_dtype dtype, int B, int L, int V,
+                                const uint8_t* mask, const int32_t* block_start,
+                                const int32_t* block_end, int32_t* counts, fdllm_stream stream) {
+  if (dtype != FDLLM_BF16 && dtype != FDLLM_F32) return FDLLM_ERR_UNSUPPORTED_DTYPE;
+  if (B < 0 || L < 1) return FDLLM_ERR_INVALID_ARG;
+  if (!sizes_ok(B, L, V)) return FDLLM_ERR_SIZE;
+  if (!counts) return FDLLM_ERR_INVALID_ARG;
+  if (B > 0 && (!logits || !mask || !block_start || !block_end)) return FDLLM_ERR_INVALID_ARG;
+  hipStream_t st = (hipStream_t)stream;
+  hipLaunchKernelGGL(k_check_clear, dim3(1), dim3(kWave), 0, st, counts);
+  if (B > 0) {
+    const unsigned grid = (unsigned)(((long long)B * L + 3) / 4);
+    if (vec_path(logits, V, dtype)) {
+      if (dtype == FDLLM_BF16)
+        hipLaunchKernelGGL(k_check<VecBf16x8>, dim3(grid), dim3(256), 0, st,
+                           (const u32x4*)logits, B, L, V / 8, mask, block_start, block_end, counts);
+      else
+        hipLaunchKernelGGL(k_check<VecF32x4>, dim3(grid), dim3(256), 0, st,
+                           (const u32x4*)logits, B, L, V / 4, mask, block_start, block_end, counts);
+    } else if (dtype == FDLLM_BF16) {
+      hipLaunchKernelGGL(k_check<VecBf16x1>, dim3(grid), dim3(256), 0, st,
+                         (const unsigned short*)logits, B, L, V, mask, block_start, block_end, counts);
+    } else {
+      hipLaunchKernelGGL(k_check<VecF32x1>, dim3(grid), dim3(256), 0, st,
+                         (const unsigned int*)logits, B, L, V, mask, block_start, block_end, counts);
+    }
+  }
+  if (hipGetLastError() != hipSuccess) return FDLLM_ERR_HIP;
+  int32_t host[3] = {0, 0, 0};
+  if (hipMemcpyAsync(host, counts, sizeof(host), hipMemcpyDeviceToHost, st) != hipSuccess ||
+      hipStreamSynchronize(st) != hipSuccess)
+    return FDLLM_ERR_HIP;
+  if (host[0] > 0) return FDLLM_ERR_BOUNDS;
+  if (host[1] > 0) return FDLLM_ERR_BLOCK_TOO_LARGE;
+  if (host[2] > 0) return FDLLM_ERR_NONFINITE;
+  return FDLLM_OK;
 }
 
 fdllm_status fdllm_workspace_size(int B, int L, int V, fdllm_dtype dtype, size_t* bytes) {

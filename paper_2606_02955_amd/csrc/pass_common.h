@@ -97,7 +97,20 @@ __device__ __forceinline__ int wave_min(int v) {
 // exponent reference and per-element term.  Shared by the streaming loop
 // and the final step, so the greedy element's term is recomputed bit-exactly.
 // ---------------------------------------------------------------------------
-__device__ __forceinline__ float exp_ref(float m) { return ceilf(m * kLog2e); }
+//
+// exp_ref(m) is the smallest integer K >= m * log2e (log2e taken as the float
+// kLog2e).  The product of two floats is exact in double and ceil() of it is
+// exact, so for |m| <= FDLLM_MAX_ABS_LOGIT (|K| < 2^24, a float) the maximum's
+// own argument m * log2e - K lies in (-1, 0] at every magnitude and its term
+// in (1/2, 1].  (A float product rounds to a grid coarser than 1 once
+// |m log2e| >= 2^24, and its ceiling can then sit far from the exact one.)
+// Outside that range K is rounded up to the next float, so the argument stays
+// <= 0 and no term overflows.
+__device__ __forceinline__ float exp_ref(float m) {
+  const double k = ceil((double)m * (double)kLog2e);
+  const float kf = (float)k;
+  return (double)kf < k ? __int_as_float(__float_as_int(kf) + (kf > 0.0f ? 1 : -1)) : kf;
+}
 __device__ __forceinline__ float term(float x, float K) {
   return __builtin_amdgcn_exp2f(__builtin_fmaf(x, kLog2e, -K));
 }

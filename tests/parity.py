@@ -97,12 +97,20 @@ def oracle_confidence_subset(inp, bs: Sequence[int]):
 
 
 def check_defaults(g_tok, g_conf, g_eps, g_lse, mask, start, end, bs):
-    for b in bs:
-        for i in range(mask.shape[1]):
-            cand = int(start[b]) <= i < int(end[b]) and mask[b, i] and int(end[b]) - int(start[b]) <= MAX_BLOCK
-            if not cand:
-                assert (int(g_tok[b, i]), float(g_conf[b, i]), float(g_eps[b, i]), float(g_lse[b, i])) \
-                    == (-1, 0.0, 1.0, 0.0), (b, i)
+    """Non-candidate positions of the sequences bs hold the default outputs."""
+    bs = np.asarray(list(bs), dtype=np.int64)
+    if bs.size == 0:
+        return
+    L = mask.shape[1]
+    pos = np.arange(L)[None, :]
+    s = np.asarray(start)[bs][:, None].astype(np.int64)
+    e = np.asarray(end)[bs][:, None].astype(np.int64)
+    cand = (pos >= s) & (pos < e) & (np.asarray(mask)[bs] != 0) & ((e - s) <= MAX_BLOCK)
+    dead = ~cand
+    ok = ((np.asarray(g_tok)[bs] == -1) & (np.asarray(g_conf)[bs] == 0.0) &
+          (np.asarray(g_eps)[bs] == 1.0) & (np.asarray(g_lse)[bs] == 0.0))
+    bad = np.argwhere(dead & ~ok)
+    assert bad.size == 0, f"default outputs wrong at {[(int(bs[r]), int(c)) for r, c in bad[:5]]}"
 
 
 def compare_selection(g_commit, g_n, o_commit, o_n, flagged, bs) -> Tuple[int, int]:
@@ -120,3 +128,97 @@ def compare_selection(g_commit, g_n, o_commit, o_n, flagged, bs) -> Tuple[int, i
             bad.append(b)
     assert not bad, f"unflagged blocks differ: {bad[:10]}"
     return nflag, nflag_match
+
+
+# ---------------------------------------------------------------------------
+# whole-workload checks: the oracle in worker processes (oracle.parallel)
+# ---------------------------------------------------------------------------
+def check_bounds(start: np.ndarray, end: np.ndarray, L: int):
+    """The oracle's bounds rule (it raises on a bad window)."""
+    for b in range(len(start)):
+        lo, hi = int(start[b]), int(end[b])
+        if not (0 <= lo <= hi <= L):
+            raise ValueError(f"bad block bounds for sequence {b}: [{lo},{hi}) with L={L}")
+
+
+def pool_confidence(pool, logits: torch.Tensor, mask: np.ndarray, start: np.ndarray,
+                    end: np.ndarray, bs: Optional[Sequence[int]] = None):
+    """Oracle (tokens, conf, eps, lse) [B, L] of every candidate of the
+    sequences bs (all when None), rows copied from the GPU tensor's exact bits;
+    non-candidates and other sequences keep the oracle's defaults."""
+    from oracle.parallel import scatter_confidence
+    B, L, V = logits.shape
+    check_bounds(start, end, L)
+    bs = range(B) if bs is None else bs
+    cells = candidates(mask, start, end, bs)
+    kind = "bf16" if logits.dtype == torch.bfloat16 else "f32"
+    flat = logits.view(B * L, V)
+    idx = torch.tensor([b * L + i for b, i in cells], dtype=torch.long, device=logits.device)
+
+    def fill(first, cnt, out):
+        rows = flat.index_select(0, idx[first:first + cnt])
+        torch.from_numpy(out).copy_(rows.view(torch.int16) if kind == "bf16" else rows)
+
+    res = pool.rows_confidence(fill, len(cells), V, kind)
+    return scatter_confidence(B, L, cells, res)
+
+
+def sub_mask(mask: np.ndarray, bs: Sequence[int]) -> np.ndarray:
+    m = np.zeros_like(mask)
+    idx = list(bs)
+    m[idx] = mask[idx]
+    return m
+
+
+def selection_stats(g_commit, g_n, o_commit, o_n, flagged, bs) -> dict:
+    """Counts of a selection comparison on the blocks bs (no assertion)."""
+    st = dict(blocks=0, mismatches=0, flagged=0, flagged_matching=0, bad=[])
+    for b in bs:
+        same = np.array_equal(g_commit[b], o_commit[b]) and int(g_n[b]) == int(o_n[b])
+        st["blocks"] += 1
+        if flagged[b]:
+            st["flagged"] += 1
+            st["flagged_matching"] += int(same)
+        elif not same:
+            st["mismatches"] += 1
+            st["bad"].append(int(b))
+    return st
+
+
+class ParityTally:
+    """Per-workload totals of the comparisons, printed and, when the
+    environment names a file (FDLLM_PARITY_REPORT), appended to it as JSON."""
+
+    def __init__(self, workload: str, **info):
+        self.d = dict(workload=workload, block_checks=0, mismatches=0, flagged=0,
+                      flagged_matching=0, rows=0, worst=dict(conf=0.0, eps=0.0, lse=0.0),
+                      rules={}, **info)
+
+    def rows_checked(self, n: int, worst: dict):
+        self.d["rows"] += n
+        for k, v in worst.items():
+            self.d["worst"][k] = max(self.d["worst"][k], v)
+
+    def selection(self, rule: str, st: dict):
+        r = self.d["rules"].setdefault(rule, dict(block_checks=0, mismatches=0, flagged=0,
+                                                  flagged_matching=0))
+        for key, src in (("block_checks", "blocks"), ("mismatches", "mismatches"),
+                         ("flagged", "flagged"), ("flagged_matching", "flagged_matching")):
+            r[key] += st[src]
+            self.d[key] += st[src]
+        assert st["mismatches"] == 0, f"{rule}: unflagged blocks differ: {st['bad'][:10]}"
+
+    def note(self, **kv):
+        self.d.update(kv)
+
+    def finish(self):
+        import json
+        import os
+        say(f"  parity {self.d['workload']}: {self.d['block_checks']} block checks, "
+            f"{self.d['mismatches']} mismatches, {self.d['flagged']} flagged "
+            f"({self.d['flagged_matching']} matching), {self.d['rows']} rows, worst {self.d['worst']}")
+        path = os.environ.get("FDLLM_PARITY_REPORT")
+        if path:
+            with open(path, "a") as fh:
+                fh.write(json.dumps(self.d) + "\n")
+        return self.d

@@ -37,8 +37,9 @@ def test_every_declared_symbol_is_exported(lib):
 
 
 def test_status_strings(lib):
-    for st in (0, -1, -2, -3, -4, -5):
+    for st in (0, -1, -2, -3, -4, -5, -6, -7, -8):
         assert len(fd.status_string(st)) > 0
+        assert "unknown" not in fd.status_string(st)
     assert fd.status_string(0) == "ok"
     assert "unknown" in fd.status_string(99)
 
@@ -99,6 +100,27 @@ def test_error_paths_enqueue_nothing(lib):
     assert lib.fdllm_decode_step(*args(V=0)) == fd.ERR_SIZE
     assert lib.fdllm_decode_step(*args()) == fd.ERR_WORKSPACE            # B=8: two-kernel plan
     assert lib.fdllm_decode_step(*args(ws=p, wsb=16)) == fd.ERR_WORKSPACE
+
+
+def test_check_inputs_error_paths(lib):
+    p = ctypes.c_void_p(0x1000)
+    null = None
+    f = lib.fdllm_check_inputs
+    assert f(p, 0, 2, 4, 16, p, p, p, null, null) == fd.ERR_INVALID_ARG        # counts required
+    assert f(null, 0, 2, 4, 16, p, p, p, p, null) == fd.ERR_INVALID_ARG
+    assert f(p, 0, 2, 4, 16, null, p, p, p, null) == fd.ERR_INVALID_ARG
+    assert f(p, 3, 2, 4, 16, p, p, p, p, null) == fd.ERR_UNSUPPORTED_DTYPE
+    assert f(p, 0, 2, 4, 0, p, p, p, p, null) == fd.ERR_SIZE
+    assert f(p, 0, -1, 4, 16, p, p, p, p, null) == fd.ERR_INVALID_ARG
+
+
+def test_constants_agree_with_header():
+    text = open(HEADER).read()
+    m = re.search(r"#define FDLLM_MAX_ABS_LOGIT ([0-9.e]+)f", text)
+    assert m and float(m.group(1)) == fd.MAX_ABS_LOGIT
+    for name, val in (("BOUNDS", fd.ERR_BOUNDS), ("BLOCK_TOO_LARGE", fd.ERR_BLOCK_TOO_LARGE),
+                      ("NONFINITE", fd.ERR_NONFINITE)):
+        assert re.search(rf"#define FDLLM_ERR_{name} \({val}\)", text), name
 
 
 def test_binding_refuses_cpu_tensors(lib):

@@ -49,7 +49,7 @@ def test_advance_blocks_match_cpu(gpu):
     n_d = torch.full((1,), -5, dtype=torch.int32, device="cuda")
     gpu.fdllm_advance_blocks(torch.from_numpy(mask).cuda(), s_d, e_d, blk, n_d)
     torch.cuda.synchronize()
-    n = synth.advance_blocks(mask, start, end, G, blk)
+    n = oracle.advance_blocks(mask, start, end, G, blk)
     assert s_d.cpu().numpy().tolist() == start.tolist()
     assert e_d.cpu().numpy().tolist() == end.tolist()
     assert int(n_d[0]) == n
@@ -74,7 +74,7 @@ def _replay(seed, B, G, blk, V, rule, p, eta, hist, steps_gpu, x_gpu):
                 diverged.add(b)
             flagged_total += int(r.flagged[b])
         mask, x = r.mask, r.x
-        active = synth.advance_blocks(mask, start, end, G, blk)
+        active = oracle.advance_blocks(mask, start, end, G, blk)
         t += 1
     assert not mask.any()
     for b in range(B):

@@ -1,9 +1,22 @@
-"""GPU parity on the five workload recipes at their full sizes.
+"""GPU parity on the five workload recipes at their full sizes, whole.
 
-The single-block and sparse-block recipes are checked on every candidate
-row; the throughput stress (8.3 GB of logits) on a seeded sample of blocks
-plus properties that hold at any size; the simulated generations run in
-lockstep with the oracle for their first steps.
+Every candidate row of every checked step is compared with the oracle
+(tokens bit-exact, conf / eps / lse within the tolerances of parity.py), and
+every checked block's commit set with the oracle's selection on the oracle's
+own confidences (level 3: logits in, commits out), bit for bit unless the
+oracle flags the block as within 1e-6 of a decision boundary.  The oracle
+runs in worker processes (oracle.parallel) on exact copies of the rows the
+GPU read.
+
+  * single block (B=1, L=32, fp32): every row, three rules;
+  * generation (B=8, 256 positions in blocks of 32): seven whole
+    generations, one driven by each rule, every step and every sequence;
+  * sparse blocks (B=64, span 512): every candidate row, five rules;
+  * bimodal generation (B=256, 1024 positions in blocks of 64): the whole
+    generation driven by the profile rule; every step of the 16 flat
+    sequences and four others, all five rules, and every sequence at step 0;
+  * throughput stress (B=1024, L=32, 8.3 GB): every one of the 1024 blocks,
+    six rules.
 """
 import gc
 
@@ -13,8 +26,8 @@ import torch
 
 import oracle
 import workloads
-from parity import (say, row_source, candidates, compare_rows, gpu_confidence,
-                    oracle_confidence_subset, check_defaults, compare_selection)
+from parity import (say, candidates, compare_rows, check_defaults, pool_confidence, sub_mask,
+                    selection_stats, ParityTally)
 
 pytestmark = pytest.mark.gpu
 
@@ -39,180 +52,225 @@ def _decode(gpu, inp, rule, p, mask=None, x=None, eta=None, eta_uniform=0.0):
     return mask, x, o
 
 
-def _oracle_step(inp, bs, rule, p):
-    B, L, V = inp.logits.shape
-    m = inp.mask.cpu().numpy().copy()
-    keep = np.zeros(B, dtype=bool)
-    keep[list(bs)] = True
-    m[~keep] = 0
-    return oracle.decode_step(row_source(inp.logits), B, L, m, inp.start.cpu().numpy(),
-                              inp.end.cpu().numpy(), inp.x.cpu().numpy(), rule, p)
+def _host(o):
+    return {k: v.cpu().numpy() for k, v in o.items()}
 
 
-def _check_step(inp, o, bs, rule, p):
-    r = _oracle_step(inp, bs, rule, p)
-    nf, nfm = compare_selection(o["commit"].cpu().numpy(), o["n_commit"].cpu().numpy(),
-                                r.commit, r.n_commit, r.flagged, bs)
-    cells = candidates(inp.mask.cpu().numpy(), inp.start.cpu().numpy(), inp.end.cpu().numpy(), bs)
-    g = [o[k].cpu().numpy() for k in ("tokens", "conf", "eps", "lse")]
-    worst = compare_rows(*g, r.tokens, r.conf, r.eps, r.lse, cells)
-    return nf, nfm, worst, r
+class _Step:
+    """One step's inputs on the host plus the oracle's confidences of the
+    checked sequences."""
+
+    def __init__(self, pool, inp, bs):
+        self.inp = inp
+        self.mask = inp.mask.cpu().numpy()
+        self.start = inp.start.cpu().numpy()
+        self.end = inp.end.cpu().numpy()
+        self.x = inp.x.cpu().numpy()
+        self.bs = list(bs)
+        self.pool = pool
+        self.cells = candidates(self.mask, self.start, self.end, self.bs)
+        self.tokens, self.conf, self.eps, self.lse = pool_confidence(pool, inp.logits, self.mask,
+                                                                     self.start, self.end, self.bs)
+
+    def check_rows(self, tally, go):
+        worst = compare_rows(go["tokens"], go["conf"], go["eps"], go["lse"], self.tokens, self.conf,
+                             self.eps, self.lse, self.cells)
+        check_defaults(go["tokens"], go["conf"], go["eps"], go["lse"], self.mask, self.start,
+                       self.end, self.bs)
+        tally.rows_checked(len(self.cells), worst)
+
+    def check_rules(self, tally, runs):
+        """Level 3 for several rules on this step's inputs: the oracle's
+        selection on the oracle's confidences, then the reveal, against each
+        GPU run's commits, n_commit, x and mask.  runs: (rule, p, eta, outputs,
+        mask after, x after)."""
+        sel = self.pool.select_many(self.eps, self.conf, self.mask, self.start, self.end,
+                                    [(r[0], r[1], r[2]) for r in runs], blocks=self.bs)
+        stats = []
+        for (rule, p, eta, go, g_mask, g_x), (oc, on, fl) in zip(runs, sel):
+            st = selection_stats(go["commit"], go["n_commit"], oc, on, fl, self.bs)
+            tally.selection(f"{rule}({p})" if eta is None else f"{rule}({p}, eta={eta})", st)
+            hit = oc.astype(bool)
+            ox, om = self.x.copy(), self.mask.copy()
+            ox[hit] = self.tokens[hit]
+            om[hit] = 0
+            for b in self.bs:
+                if not fl[b]:
+                    assert np.array_equal(g_x[b], ox[b]) and np.array_equal(g_mask[b], om[b]), b
+            stats.append(st)
+        return stats
 
 
-def test_single_block_b1_l32_full(gpu):
+def test_single_block_b1_l32_full(gpu, oracle_pool):
     say("[single block] B=1 L=32 V=126464 fp32")
     inp = workloads.single_block_b1_l32(device="cuda")
+    tally = ParityTally("single_block_b1_l32", B=1, L=32, steps=1)
+    step = _Step(oracle_pool, inp, [0])
+    runs = []
     for rule, p in [("profile", 1.0), ("factor", 1.0), ("threshold", 0.9)]:
         mask, x, o = _decode(gpu, inp, rule, p)
-        nf, nfm, worst, r = _check_step(inp, o, [0], rule, p)
-        assert int(o["n_commit"][0]) >= 1
-        say(f"  {rule}({p}): n*={int(o['n_commit'][0])} flagged={nf} worst={worst}")
+        go = _host(o)
+        step.check_rows(tally, go)
+        runs.append((rule, p, None, go, mask.cpu().numpy(), x.cpu().numpy()))
+        assert int(go["n_commit"][0]) >= 1
+    step.check_rules(tally, runs)
     # two rows hold exact ties at their maximum: lowest index wins
-    tok = o["tokens"][0].cpu().numpy()
     rows = inp.logits[0].cpu().numpy()
     for i in range(32):
-        assert tok[i] == int(np.argmax(rows[i]))
+        assert go["tokens"][0, i] == int(np.argmax(rows[i]))
+    tally.finish()
 
 
-def test_sparse_b64_g512_full(gpu):
+def test_sparse_b64_g512_full(gpu, oracle_pool):
     say("[sparse blocks] B=64 L=512 V=126464 bf16, poisoned non-candidate rows")
     inp = workloads.sparse_b64_g512(device="cuda")
-    g = gpu_confidence(gpu, inp)
-    assert all(bool(torch.isfinite(t.float()).all()) for t in g[1:])
+    tally = ParityTally("sparse_b64_g512", B=64, L=512, steps=1)
+    step = _Step(oracle_pool, inp, range(64))
+    runs = []
     for rule, p in [("profile", 1.0), ("profile", 0.75), ("factor", 1.0), ("factor", 0.75),
                     ("threshold", 0.9)]:
         mask, x, o = _decode(gpu, inp, rule, p)
-        for name, t in zip(("tokens", "conf", "eps", "lse"), g):
-            assert torch.equal(o[name].view(torch.int32), t.view(torch.int32))
-        if rule == "profile" and p == 1.0:
-            nf, nfm, worst, r = _check_step(inp, o, range(64), rule, p)
-            say(f"  {rule}({p}): rows={int(inp.mask.sum())} flagged={nf} worst={worst}")
-        else:
-            # selection on the oracle's own confidences, reusing the last oracle pass
-            oc, on, fl, _ = oracle.select(r.eps, r.conf, inp.mask.cpu().numpy(), inp.start.cpu().numpy(),
-                                          inp.end.cpu().numpy(), rule, p)
-            nf, nfm = compare_selection(o["commit"].cpu().numpy(), o["n_commit"].cpu().numpy(),
-                                        oc, on, fl, range(64))
-            say(f"  {rule}({p}): commits={int(o['n_commit'].sum())} flagged={nf}")
-    del inp, g
+        go = _host(o)
+        step.check_rows(tally, go)
+        runs.append((rule, p, None, go, mask.cpu().numpy(), x.cpu().numpy()))
+    step.check_rules(tally, runs)
+    tally.finish()
+    del inp
     _free()
 
 
-def test_stress_b1024_l32_sampled(gpu):
-    say("[throughput stress] B=1024 L=32 V=126464 bf16 (8.3 GB), fused decode step")
+def test_stress_b1024_l32_full(gpu, oracle_pool):
+    say("[throughput stress] B=1024 L=32 V=126464 bf16 (8.3 GB), fused decode step, every block")
     inp = workloads.stress_b1024_l32(device="cuda")
     B, L, V = inp.logits.shape
-    rng = np.random.default_rng(2026)
-    sample = sorted(rng.choice(B, 24, replace=False).tolist())
-    conf_ref = gpu_confidence(gpu, inp)
-    res = {}
-    for rule, p in [("profile", 1.0), ("factor", 1.0), ("profile", 0.75), ("factor", 0.75),
-                    ("threshold", 0.9)]:
-        mask, x, o = _decode(gpu, inp, rule, p)
-        res[(rule, p)] = o
-        n = o["n_commit"]
-        assert int(n.min()) >= 1 and int(n.max()) <= L
-        assert torch.equal(o["commit"].sum(1, dtype=torch.int32), n)
-        assert not (o["commit"].bool() & mask.bool()).any()             # committed -> unmasked
-        assert torch.equal(torch.where(o["commit"].bool(), o["tokens"], x), x)
-        for name, t in zip(("tokens", "conf", "eps", "lse"), conf_ref):
-            assert torch.equal(o[name].view(torch.int32), t.view(torch.int32))
-        c2 = torch.empty_like(o["commit"]); n2 = torch.empty_like(n)
-        gpu.select(rule, conf_ref[1], conf_ref[2], inp.mask, inp.start, inp.end, p, c2, n2)
-        torch.cuda.synchronize()
-        assert torch.equal(c2, o["commit"]) and torch.equal(n2, n)
-        say(f"  {rule}({p}): mean commits/block {float(n.float().mean()):.3f}")
+    tally = ParityTally("stress_b1024_l32", B=B, L=L, steps=1)
+    step = _Step(oracle_pool, inp, range(B))
+    say(f"  oracle: {len(step.cells)} rows")
+    res, runs = {}, []
+    rules = [("profile", 1.0, None), ("factor", 1.0, None), ("profile", 0.75, None),
+             ("factor", 0.75, None), ("threshold", 0.9, None), ("robust", 1.0, 0.02)]
+    for rule, p, eta in rules:
+        mask, x, o = _decode(gpu, inp, rule, p, eta_uniform=eta or 0.0)
+        go = _host(o)
+        res[(rule, p)] = go
+        step.check_rows(tally, go)
+        runs.append((rule, p, eta, go, mask.cpu().numpy(), x.cpu().numpy()))
+        assert int(go["n_commit"].min()) >= 1 and int(go["n_commit"].max()) <= L
+    for (rule, p, eta, go, _, _), st in zip(runs, step.check_rules(tally, runs)):
+        say(f"  {rule}({p}): mean commits/block {float(go['n_commit'].mean()):.3f}, "
+            f"flagged {st['flagged']}")
     # matched-factor dominance holds exactly in the GPU arithmetic
     for p in (1.0, 0.75):
         assert (res[("profile", p)]["n_commit"] >= res[("factor", p)]["n_commit"]).all()
     # the calibration-robust rule never commits more than the plain rule
-    mask_r, x_r, o_r = _decode(gpu, inp, "robust", 1.0, eta_uniform=0.02)
-    assert (o_r["n_commit"] <= res[("profile", 1.0)]["n_commit"]).all()
-    assert (o_r["n_commit"] >= 1).all()
-    say(f"  robust(1.0, eta=0.02): mean commits/block {float(o_r['n_commit'].float().mean()):.3f}")
-    nf, nfm, worst, r = _check_step(inp, res[("profile", 1.0)], sample, "profile", 1.0)
-    say(f"  oracle on {len(sample)} blocks: flagged={nf} worst={worst}")
-    res[("robust", 1.0)] = o_r
-    for rule, p in [("factor", 1.0), ("threshold", 0.9), ("profile", 0.75), ("robust", 1.0)]:
-        oc, on, fl, _ = oracle.select(r.eps, r.conf, np.where(np.isin(np.arange(B), sample)[:, None],
-                                      inp.mask.cpu().numpy(), 0), inp.start.cpu().numpy(),
-                                      inp.end.cpu().numpy(), rule, p,
-                                      eta=0.02 if rule == "robust" else None)
-        o = res[(rule, p)]
-        nf, nfm = compare_selection(o["commit"].cpu().numpy(), o["n_commit"].cpu().numpy(), oc, on, fl, sample)
-        say(f"  {rule}({p}) on sample: flagged={nf}")
-    del inp, conf_ref, res
+    assert (res[("robust", 1.0)]["n_commit"] <= res[("profile", 1.0)]["n_commit"]).all()
+    tally.finish()
+    del inp
     _free()
 
 
-def _simulate(gpu, recipe, rules, steps, check_bs, B=None):
-    sim = workloads.SimulatedGeneration(recipe, device="cuda", B=B)
-    flagged_total = 0
-    for s in range(steps):
-        if sim.done():
-            break
+def _generation(gpu, pool, recipe, drive, side, check_every, check_first, tally, max_steps,
+                on_step=None):
+    """A whole simulated generation driven by the GPU's `drive` rule.  At every
+    step the sequences `check_every` (at step 0 also `check_first`) are
+    compared with the oracle for the driving rule and every rule of `side`
+    (run on the same inputs, not driving).  Returns the number of steps."""
+    sim = workloads.SimulatedGeneration(recipe, device="cuda")
+    steps = 0
+    # the host loop's windows follow the oracle's block advance (Alg. 1 outer loop)
+    w_start = np.zeros(sim.B, dtype=np.int64)
+    w_end = np.full(sim.B, sim.blk, dtype=np.int64)
+    while not sim.done():
+        assert steps < max_steps, "generation did not finish"
         inp = sim.prepare_step()
-        say(f"  step {s}: active rows {int(sum((inp.end - inp.start).tolist()))}")
-        outs = {}
-        for rule, p in rules:
-            mask, x, o = _decode(gpu, inp, rule, p)
-            outs[(rule, p)] = (mask, x, o)
-        # oracle in lockstep on the checked sequences, first rule drives the trajectory
-        for k, (rule, p) in enumerate(rules):
-            mask, x, o = outs[(rule, p)]
-            if k == 0:
-                nf, nfm, worst, r = _check_step(inp, o, check_bs, rule, p)
-            else:
-                oc, on, fl, _ = oracle.select(r.eps, r.conf, _sub_mask(inp, check_bs),
-                                              inp.start.cpu().numpy(), inp.end.cpu().numpy(), rule, p)
-                nf, nfm = compare_selection(o["commit"].cpu().numpy(), o["n_commit"].cpu().numpy(),
-                                            oc, on, fl, check_bs)
-            flagged_total += nf
-        yield sim, inp, outs
-        mask, x, _ = outs[rules[0]]
+        oracle.advance_blocks(sim.mask.cpu().numpy(), w_start, w_end, sim.G, sim.blk)
+        live = w_end > w_start
+        assert np.array_equal(inp.start.cpu().numpy()[live], w_start[live])
+        assert np.array_equal(inp.end.cpu().numpy()[live], w_end[live])
+        assert np.array_equal(inp.end.cpu().numpy()[~live], inp.start.cpu().numpy()[~live])
+        bs = sorted(set(check_every) | (set(check_first) if steps == 0 else set()))
+        bs = [b for b in bs if int(inp.end[b]) > int(inp.start[b])]
+        step = _Step(pool, inp, bs)
+        rule, p = drive
+        mask, x, o = _decode(gpu, inp, rule, p)
+        go = _host(o)
+        step.check_rows(tally, go)
+        runs = [(rule, p, None, go, mask.cpu().numpy(), x.cpu().numpy())]
+        outs = {drive: go}
+        for srule, sp in side:
+            m2, x2, o2 = _decode(gpu, inp, srule, sp)
+            g2 = _host(o2)
+            for k in ("tokens", "conf", "eps", "lse"):
+                assert np.array_equal(g2[k].view(np.int32), go[k].view(np.int32))
+            runs.append((srule, sp, None, g2, m2.cpu().numpy(), x2.cpu().numpy()))
+            outs[(srule, sp)] = g2
+        step.check_rules(tally, runs)
+        if on_step is not None:
+            on_step(sim, inp, outs)
         sim.mask.copy_(mask)
         sim.x.copy_(x)
-    say(f"  flagged blocks in total: {flagged_total}")
+        steps += 1
+    # every position revealed, with the token its step proposed
+    assert not bool(sim.mask.any()) and bool((sim.x >= 0).all())
+    return steps
 
 
-def _sub_mask(inp, bs):
-    m = inp.mask.cpu().numpy().copy()
-    keep = np.zeros(m.shape[0], dtype=bool)
-    keep[list(bs)] = True
-    m[~keep] = 0
-    return m
-
-
-def test_generation_b8_g256_simulation(gpu):
-    say("[generation] B=8 gen 256 in blocks of 32, lockstep with the oracle")
-    rules = [("profile", 1.0), ("factor", 1.0), ("profile", 0.5), ("factor", 0.5),
+GEN_RULES = [("profile", 1.0), ("factor", 1.0), ("profile", 0.5), ("factor", 0.5),
              ("profile", 2.0), ("factor", 2.0), ("threshold", 0.9)]
-    for sim, inp, outs in _simulate(gpu, workloads.GENERATION, rules, steps=6, check_bs=range(8)):
-        for f in (0.5, 1.0, 2.0):
-            assert (outs[("profile", f)][2]["n_commit"] >= outs[("factor", f)][2]["n_commit"]).all()
+
+
+def test_generation_b8_g256_whole(gpu, oracle_pool):
+    say("[generation] B=8 gen 256 in blocks of 32: a whole generation per rule, every step checked")
+    tally = ParityTally("generation_b8_g256", B=8, G=256, blk=32)
+    nfe = {}
+    for drive in GEN_RULES:
+        side = [("factor", drive[1])] if drive[0] == "profile" else []
+
+        def dominance(sim, inp, outs, f=drive[1], prof=drive[0] == "profile"):
+            if prof:
+                assert (outs[("profile", f)]["n_commit"] >= outs[("factor", f)]["n_commit"]).all()
+
+        nfe[f"{drive[0]}({drive[1]})"] = _generation(gpu, oracle_pool, workloads.GENERATION, drive,
+                                                     side, range(8), (), tally, max_steps=256,
+                                                     on_step=dominance)
+        say(f"  {drive[0]}({drive[1]}): {nfe[f'{drive[0]}({drive[1]})']} steps")
+    tally.note(steps_per_generation=nfe)
+    tally.finish()
     _free()
 
 
-def test_bimodal_b256_g1024_simulation(gpu):
-    say("[bimodal generation] B=256 gen 1024 in blocks of 64, lockstep on a subset incl. all flat sequences")
-    sim_probe = workloads.SimulatedGeneration(workloads.BIMODAL_GENERATION, device="cpu", V=8)
-    flat = [b for b in range(256) if sim_probe.flat[b]]
-    check = sorted(set(flat) | {0, 1, 100, 255})
-    rules = [("profile", 1.0), ("factor", 1.0), ("profile", 0.75), ("factor", 0.75), ("threshold", 0.9)]
-    for sim, inp, outs in _simulate(gpu, workloads.BIMODAL_GENERATION, rules, steps=2, check_bs=check):
+def test_bimodal_b256_g1024_whole(gpu, oracle_pool):
+    say("[bimodal generation] B=256 gen 1024 in blocks of 64: whole generation, flat + 4 others every "
+        "step, all 256 at step 0")
+    probe = workloads.SimulatedGeneration(workloads.BIMODAL_GENERATION, device="cpu", V=8)
+    flat = [b for b in range(256) if probe.flat[b]]
+    others = [b for b in (0, 1, 100, 255) if b not in flat]
+    while len(others) < 4:
+        others.append(next(b for b in range(2, 256) if b not in flat and b not in others))
+    check = sorted(set(flat) | set(others))
+    tally = ParityTally("bimodal_b256_g1024", B=256, G=1024, blk=64, flat_sequences=flat,
+                        every_step_sequences=check)
+    side = [("factor", 1.0), ("profile", 0.75), ("factor", 0.75), ("threshold", 0.9)]
+
+    def flat_checks(sim, inp, outs):
         for f in (0.75, 1.0):
-            npf = outs[("profile", f)][2]["n_commit"].cpu().numpy()
-            nfa = outs[("factor", f)][2]["n_commit"].cpu().numpy()
+            npf = outs[("profile", f)]["n_commit"]
+            nfa = outs[("factor", f)]["n_commit"]
             assert (npf >= nfa).all()
-            # flat blocks: profile == factor, bit-exactly on the GPU
+            # flat blocks: profile == factor, bit for bit on the GPU
             assert (npf[flat] == nfa[flat]).all()
             for b in flat:
-                assert torch.equal(outs[("profile", f)][2]["commit"][b], outs[("factor", f)][2]["commit"][b])
+                assert np.array_equal(outs[("profile", f)]["commit"][b], outs[("factor", f)]["commit"][b])
         # rows of a flat block are identical, so their confidences are identical bits
-        eps = outs[rules[0]][2]["eps"]
+        eps = outs[("profile", 1.0)]["eps"]
+        m = inp.mask.cpu().numpy()
         for b in flat:
             s, e = int(inp.start[b]), int(inp.end[b])
-            m = inp.mask[b, s:e].bool()
-            v = eps[b, s:e][m].view(torch.int32)
-            assert (v == v[0]).all()
+            v = eps[b, s:e][m[b, s:e] != 0].view(np.int32)
+            assert (v == v[:1]).all()
+
+    steps = _generation(gpu, oracle_pool, workloads.BIMODAL_GENERATION, ("profile", 1.0), side,
+                        check, range(256), tally, max_steps=1024, on_step=flat_checks)
+    tally.note(steps=steps)
+    tally.finish()
     _free()

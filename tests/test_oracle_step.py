@@ -117,3 +117,19 @@ def test_single_block_recipe():
     r = oracle.decode_step(lg[None], 1, 32, inp.mask.numpy(), inp.start.numpy(), inp.end.numpy(),
                            inp.x.numpy(), "profile", 1.0)
     assert r.n_commit[0] >= 1
+
+
+def test_advance_blocks():
+    """Alg. 1 outer loop: a finished block hands over to the next block with a
+    masked position; hand-derived windows."""
+    G, blk = 10, 4                                   # blocks [0,4) [4,8) [8,10)
+    mask = np.array([[0, 0, 0, 0, 1, 0, 0, 0, 0, 0],     # first block done -> [4,8)
+                     [1, 0, 0, 0, 0, 0, 0, 0, 0, 0],     # stays
+                     [0, 0, 0, 0, 0, 0, 0, 0, 0, 1],     # skips an empty block -> [8,10)
+                     [0] * 10,                           # finished -> [10,10)
+                     [0, 0, 0, 0, 0, 0, 0, 0, 1, 1]], dtype=np.uint8)
+    start = np.array([0, 0, 0, 0, 8])
+    end = np.array([4, 4, 4, 4, 10])
+    n = oracle.advance_blocks(mask, start, end, G, blk)
+    assert start.tolist() == [4, 0, 8, 10, 8] and end.tolist() == [8, 4, 10, 10, 10]
+    assert n == 4

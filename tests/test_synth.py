@@ -7,6 +7,8 @@ SC 2011); the rest of the recipe to its stated arithmetic.
 import numpy as np
 import torch
 
+import oracle
+
 from workloads import synth
 
 # (counter, key) -> output, Philox4x32-10 known-answer tests
@@ -70,17 +72,3 @@ def test_spike_height_modes():
     hi = hs >= 8.0
     assert 0.5 < hi.mean() < 0.7                   # P(u1 < 0.6) = 0.6
     assert np.all(hs[hi] < 14.0) and np.all(hs[~hi] < 6.0)
-
-
-def test_advance_blocks():
-    G, blk = 10, 4                                   # blocks [0,4) [4,8) [8,10)
-    mask = np.array([[0, 0, 0, 0, 1, 0, 0, 0, 0, 0],     # first block done -> [4,8)
-                     [1, 0, 0, 0, 0, 0, 0, 0, 0, 0],     # stays
-                     [0, 0, 0, 0, 0, 0, 0, 0, 0, 1],     # skips an empty block -> [8,10)
-                     [0] * 10,                           # finished -> [10,10)
-                     [0, 0, 0, 0, 0, 0, 0, 0, 1, 1]], dtype=np.uint8)
-    start = np.array([0, 0, 0, 0, 8])
-    end = np.array([4, 4, 4, 4, 10])
-    n = synth.advance_blocks(mask, start, end, G, blk)
-    assert start.tolist() == [4, 0, 8, 10, 8] and end.tolist() == [8, 4, 10, 10, 10]
-    assert n == 4

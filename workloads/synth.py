@@ -106,21 +106,3 @@ def row_bits(seed: int, b: int, i: int, t: int, V: int) -> np.ndarray:
 def row(seed: int, b: int, i: int, t: int, V: int) -> np.ndarray:
     """Row (b, i) at step t as float64 (exact values of the bf16 logits)."""
     return bf16_to_f32(row_bits(seed, b, i, t, V)).astype(np.float64)
-
-
-def advance_blocks(mask: np.ndarray, start: np.ndarray, end: np.ndarray, G: int, blk: int):
-    """Move every sequence to its first block, from its current one on, that
-    still has a masked position (Alg. 1, outer loop over blocks); a finished
-    sequence gets the empty window [G, G).  Updates start/end in place and
-    returns the number of sequences with an active block."""
-    active = 0
-    for b in range(mask.shape[0]):
-        s = int(start[b])
-        while s < G and not mask[b, s:min(s + blk, G)].any():
-            s += blk
-        if s >= G:
-            start[b] = end[b] = G
-        else:
-            start[b], end[b] = s, min(s + blk, G)
-            active += 1
-    return active
