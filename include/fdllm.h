@@ -87,9 +87,12 @@ typedef int fdllm_status;
 #define FDLLM_ERR_BLOCK_TOO_LARGE (-7)   /* fdllm_check_inputs: end - start > FDLLM_MAX_BLOCK */
 #define FDLLM_ERR_NONFINITE (-8)         /* fdllm_check_inputs: a candidate logit is NaN,
                                             inf or beyond FDLLM_MAX_ABS_LOGIT           */
+#define FDLLM_ERR_SCRATCH (-9)           /* fdllm_decode_step_static: the call needs more
+                                            than FDLLM_STATIC_SCRATCH_BYTES of scratch  */
 
 #define FDLLM_MAX_BLOCK 1024
 #define FDLLM_MAX_ABS_LOGIT 1.0e7f
+#define FDLLM_STATIC_SCRATCH_BYTES (8u << 20)   /* fdllm_decode_step_static, per GPU */
 
 /*
  * Greedy token, confidence, complement and log-sum-exp of every candidate
@@ -200,6 +203,35 @@ fdllm_status fdllm_decode_step(const void* logits, fdllm_dtype dtype, int B, int
                                float eta_uniform, int32_t* tokens, float* conf, float* eps,
                                float* lse, uint8_t* commit, int32_t* n_commit, void* workspace,
                                size_t workspace_bytes, fdllm_stream stream);
+
+/*
+ * fdllm_decode_step for callers that cannot allocate device memory (code under
+ * HIP graph capture, tight serving loops, harnesses that forbid allocation):
+ * the same step, with the same arguments minus the workspace, the same plans
+ * and bitwise the same results as fdllm_decode_step given a workspace of
+ * fdllm_workspace_size() bytes.  The scratch it needs instead lives in the
+ * library: a static array of FDLLM_STATIC_SCRATCH_BYTES (8 MiB) on every GPU
+ * the library runs on, held until the process ends.  The call allocates and
+ * frees nothing.
+ *   Sizes whose workspace exceeds FDLLM_STATIC_SCRATCH_BYTES are refused with
+ *   FDLLM_ERR_SCRATCH (nothing enqueued).  Batches of 128 sequences or more
+ *   need no scratch at all; smaller ones need 12 B per position of the span
+ *   (when tokens, conf or eps are not given) plus up to 384 B per position of
+ *   blocks of at most 64 positions.
+ *   Every call on one GPU uses that GPU's one array: calls that overlap on one
+ *   GPU (other streams, other threads) race and must be serialised by the
+ *   caller.  The array keeps the last call's contents; the step needs none of
+ *   them (its scratch needs no initialisation).
+ *   The first call on a device, with that device current, looks up the
+ *   array's device address (hipGetSymbolAddress) once; later calls on that
+ *   device reuse it.
+ */
+fdllm_status fdllm_decode_step_static(const void* logits, fdllm_dtype dtype, int B, int L, int V,
+                                      uint8_t* mask, const int32_t* block_start,
+                                      const int32_t* block_end, int32_t* x, fdllm_selector sel,
+                                      float param, const float* eta, float eta_uniform,
+                                      int32_t* tokens, float* conf, float* eps, float* lse,
+                                      uint8_t* commit, int32_t* n_commit, fdllm_stream stream);
 
 /*
  * ---------------------------------------------------------------------------

@@ -26,15 +26,17 @@ MAX_BLOCK = 1024
 
 OK = 0
 ERR_INVALID_ARG, ERR_UNSUPPORTED_DTYPE, ERR_SIZE, ERR_WORKSPACE, ERR_HIP = -1, -2, -3, -4, -5
-ERR_BOUNDS, ERR_BLOCK_TOO_LARGE, ERR_NONFINITE = -6, -7, -8
+ERR_BOUNDS, ERR_BLOCK_TOO_LARGE, ERR_NONFINITE, ERR_SCRATCH = -6, -7, -8, -9
 MAX_ABS_LOGIT = 1.0e7
+STATIC_SCRATCH_BYTES = 8 << 20
 
 EXPORTS = ("fdllm_confidence", "fdllm_select_profile", "fdllm_select_factor",
            "fdllm_select_threshold", "fdllm_select_robust", "fdllm_reveal", "fdllm_decode_step",
            "fdllm_workspace_size", "fdllm_status_string", "fdllm_synth_logits",
            "fdllm_advance_blocks", "fdllm_generation_workspace_size", "fdllm_generation_create",
            "fdllm_generation_run", "fdllm_generation_destroy", "fdllm_lmhead_workspace_size",
-           "fdllm_lmhead_confidence", "fdllm_lmhead_decode_step", "fdllm_check_inputs")
+           "fdllm_lmhead_confidence", "fdllm_lmhead_decode_step", "fdllm_check_inputs",
+           "fdllm_decode_step_static")
 
 
 class GenerationDesc(ctypes.Structure):
@@ -80,6 +82,8 @@ def load(path: Optional[str] = None) -> ctypes.CDLL:
     lib.fdllm_reveal.argtypes = [vp, vp, vp, vp, i32, i32, vp]
     lib.fdllm_decode_step.argtypes = [vp, i32, i32, i32, i32, vp, vp, vp, vp, i32, f32, vp, f32,
                                       vp, vp, vp, vp, vp, vp, vp, sz, vp]
+    lib.fdllm_decode_step_static.argtypes = [vp, i32, i32, i32, i32, vp, vp, vp, vp, i32, f32, vp,
+                                             f32, vp, vp, vp, vp, vp, vp, vp]
     lib.fdllm_check_inputs.argtypes = [vp, i32, i32, i32, i32, vp, vp, vp, vp, vp]
     lib.fdllm_workspace_size.argtypes = [i32, i32, i32, i32, ctypes.POINTER(sz)]
     lib.fdllm_status_string.argtypes = [i32]
@@ -97,7 +101,7 @@ def load(path: Optional[str] = None) -> ctypes.CDLL:
     lib.fdllm_generation_run.argtypes = [vp, vp, ctypes.POINTER(i32)]
     lib.fdllm_generation_destroy.argtypes = [vp]
     for name in ("fdllm_confidence", "fdllm_reveal", "fdllm_decode_step", "fdllm_workspace_size",
-                 "fdllm_check_inputs",
+                 "fdllm_decode_step_static", "fdllm_check_inputs",
                  "fdllm_synth_logits", "fdllm_advance_blocks", "fdllm_generation_workspace_size",
                  "fdllm_lmhead_workspace_size", "fdllm_lmhead_confidence", "fdllm_lmhead_decode_step",
                  "fdllm_generation_create", "fdllm_generation_run", "fdllm_generation_destroy"):
@@ -234,6 +238,25 @@ def fdllm_decode_step(logits, mask, block_start, block_end, x, selector: str, pa
         ws_ptr, ws_bytes, _stream(logits.device))
     _check(st, "fdllm_decode_step")
     return workspace
+
+
+def fdllm_decode_step_static(logits, mask, block_start, block_end, x, selector: str, param: float,
+                             tokens=None, conf=None, eps=None, lse=None, commit=None, n_commit=None,
+                             eta=None, eta_uniform: float = 0.0):
+    """fdllm_decode_step with the library's static scratch (no workspace)."""
+    B, L, V = logits.shape
+    if selector not in SELECTORS:
+        raise ValueError(f"selector must be one of {sorted(SELECTORS)}")
+    st = load().fdllm_decode_step_static(
+        _ptr(logits, name="logits"), _dtype_code(logits), B, L, V,
+        _ptr(mask, torch.uint8, (B, L), "mask"), _ptr(block_start, torch.int32, (B,), "block_start"),
+        _ptr(block_end, torch.int32, (B,), "block_end"), _ptr(x, torch.int32, (B, L), "x"),
+        SELECTORS[selector], float(param), _ptr(eta, torch.float32, (B, L), "eta"), float(eta_uniform),
+        _ptr(tokens, torch.int32, (B, L), "tokens"), _ptr(conf, torch.float32, (B, L), "conf"),
+        _ptr(eps, torch.float32, (B, L), "eps"), _ptr(lse, torch.float32, (B, L), "lse"),
+        _ptr(commit, torch.uint8, (B, L), "commit"), _ptr(n_commit, torch.int32, (B,), "n_commit"),
+        _stream(logits.device))
+    _check(st, "fdllm_decode_step_static")
 
 
 def fdllm_check_inputs(logits, mask, block_start, block_end, counts=None):

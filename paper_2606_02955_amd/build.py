@@ -16,6 +16,7 @@ ROOT = os.path.dirname(PKG)
 SRC = os.path.join(PKG, "csrc", "fdllm.hip")
 LOOP_SRC = os.path.join(PKG, "csrc", "loop.hip")
 LMHEAD_SRC = os.path.join(PKG, "csrc", "lmhead.hip")
+STATIC_SRC = os.path.join(PKG, "csrc", "decode_static.hip")
 INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(PKG, "libfdllm.so")
 BENCH_SRC = os.path.join(PKG, "csrc", "stream_read.hip")
@@ -61,7 +62,7 @@ def _compile(srcs, lib: str, verbose: bool, extra=()) -> str:
 def build(verbose: bool = False, extra=()) -> str:
     """Compile libfdllm.so and libfdllm_bench.so (always recompiles both)."""
     _compile([BENCH_SRC], BENCH_LIB, verbose)
-    return _compile([SRC, LMHEAD_SRC, LOOP_SRC], LIB, verbose, extra)
+    return _compile([SRC, LMHEAD_SRC, LOOP_SRC, STATIC_SRC], LIB, verbose, extra)
 
 
 if __name__ == "__main__":

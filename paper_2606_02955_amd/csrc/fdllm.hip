@@ -1176,6 +1176,7 @@ const char* fdllm_status_string(fdllm_status st) {
     case FDLLM_ERR_BOUNDS: return "a block window lies outside [0, L] (start > end, start < 0 or end > L)";
     case FDLLM_ERR_BLOCK_TOO_LARGE: return "a block window is longer than FDLLM_MAX_BLOCK positions";
     case FDLLM_ERR_NONFINITE: return "a candidate logit is NaN, inf or beyond FDLLM_MAX_ABS_LOGIT";
+    case FDLLM_ERR_SCRATCH: return "the call needs more than the library's static scratch (FDLLM_STATIC_SCRATCH_BYTES)";
     default: return "unknown status";
   }
 }

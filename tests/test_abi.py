@@ -37,7 +37,7 @@ def test_every_declared_symbol_is_exported(lib):
 
 
 def test_status_strings(lib):
-    for st in (0, -1, -2, -3, -4, -5, -6, -7, -8):
+    for st in (0, -1, -2, -3, -4, -5, -6, -7, -8, -9):
         assert len(fd.status_string(st)) > 0
         assert "unknown" not in fd.status_string(st)
     assert fd.status_string(0) == "ok"
@@ -114,12 +114,32 @@ def test_check_inputs_error_paths(lib):
     assert f(p, 0, -1, 4, 16, p, p, p, p, null) == fd.ERR_INVALID_ARG
 
 
+def test_static_decode_step_error_paths(lib):
+    p = ctypes.c_void_p(0x1000)
+    null = None
+    args = lambda **kw: [kw.get("logits", p), kw.get("dt", 0), kw.get("B", 8), kw.get("L", 32),
+                         kw.get("V", 64), kw.get("mask", p), p, p, kw.get("x", p), kw.get("sel", 2),
+                         1.0, null, kw.get("eta_u", 0.0), null, null, null, null, null, null, null]
+    f = lib.fdllm_decode_step_static
+    assert f(*args(sel=7)) == fd.ERR_INVALID_ARG
+    assert f(*args(sel=3, eta_u=float("nan"))) == fd.ERR_INVALID_ARG
+    assert f(*args(dt=9)) == fd.ERR_UNSUPPORTED_DTYPE
+    assert f(*args(logits=null)) == fd.ERR_INVALID_ARG
+    assert f(*args(x=null)) == fd.ERR_INVALID_ARG
+    assert f(*args(V=0)) == fd.ERR_SIZE
+    # a small batch over a long span needs 12 B per slot of scratch: beyond the static array
+    assert f(*args(B=64, L=100000)) == fd.ERR_SCRATCH
+    assert f(*args(B=0)) == 0
+
+
 def test_constants_agree_with_header():
     text = open(HEADER).read()
     m = re.search(r"#define FDLLM_MAX_ABS_LOGIT ([0-9.e]+)f", text)
     assert m and float(m.group(1)) == fd.MAX_ABS_LOGIT
+    m = re.search(r"#define FDLLM_STATIC_SCRATCH_BYTES \(8u << 20\)", text)
+    assert m and fd.STATIC_SCRATCH_BYTES == 8 << 20
     for name, val in (("BOUNDS", fd.ERR_BOUNDS), ("BLOCK_TOO_LARGE", fd.ERR_BLOCK_TOO_LARGE),
-                      ("NONFINITE", fd.ERR_NONFINITE)):
+                      ("NONFINITE", fd.ERR_NONFINITE), ("SCRATCH", fd.ERR_SCRATCH)):
         assert re.search(rf"#define FDLLM_ERR_{name} \({val}\)", text), name
 
 
