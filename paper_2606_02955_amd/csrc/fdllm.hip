@@ -62,6 +62,9 @@
 #ifndef FDLLM_TARGET_WAVES
 #define FDLLM_TARGET_WAVES 16384  // small batches: split rows until about this many waves stream
 #endif
+#ifndef FDLLM_FUSED_MIN_B
+#define FDLLM_FUSED_MIN_B 128     // batches from this size run one workgroup per sequence
+#endif
 #ifndef FDLLM_WAVES_PER_EU
 #define FDLLM_WAVES_PER_EU 0   // minimum waves per SIMD the fused kernel is compiled for (0: no hint)
 #endif
@@ -948,7 +951,7 @@ struct Plan {
   int parts;    // decode step with a workspace: split over split / 4 workgroups (0: no)
 };
 
-constexpr int kFusedMinB = 128;
+constexpr int kFusedMinB = FDLLM_FUSED_MIN_B;
 constexpr int kFusedWaves = FDLLM_FUSED_WAVES;   // waves per workgroup in the fused kernel
 constexpr int kTargetWaves = FDLLM_TARGET_WAVES;   // row-streaming waves the split aims for
 

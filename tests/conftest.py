@@ -18,6 +18,8 @@ def pytest_collection_finish(session):
     # The oracle's worker processes are spawned here, after collection and
     # before any test initialises the GPU runtime, and only when a selected
     # test asks for them.
+    if session.config.option.collectonly:
+        return
     if any("oracle_pool" in getattr(item, "fixturenames", ()) for item in session.items):
         from oracle.parallel import OraclePool
         _POOL["pool"] = OraclePool()
