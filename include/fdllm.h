@@ -67,14 +67,20 @@ extern "C" {
 /* A hipStream_t (same underlying type); NULL selects the null stream. */
 typedef struct ihipStream_t* fdllm_stream;
 
-typedef enum { FDLLM_BF16 = 0, FDLLM_F32 = 1 } fdllm_dtype;
+/* Logits element type.  Plain int, so that any value a caller passes is a
+ * value of the type (an out-of-range value of a C++ enum would not be, and the
+ * range check that rejects it could then be compiled away). */
+typedef int fdllm_dtype;
+enum { FDLLM_BF16 = 0, FDLLM_F32 = 1 };
 
-typedef enum {
+/* Selection rule (plain int, as fdllm_dtype). */
+typedef int fdllm_selector;
+enum {
   FDLLM_SEL_THRESHOLD = 0, /* commit every c >= tau, else the single highest        */
   FDLLM_SEL_FACTOR = 1,    /* largest n with (n+1)(1 - c_(n)) < f                   */
   FDLLM_SEL_PROFILE = 2,   /* largest n with G_n > 1 - f (Frechet profile rule)     */
   FDLLM_SEL_ROBUST = 3     /* profile rule on c_low = max(0, c - eta) (robust rule) */
-} fdllm_selector;
+};
 
 typedef int fdllm_status;
 #define FDLLM_OK 0
@@ -214,7 +220,7 @@ fdllm_status fdllm_decode_step(const void* logits, fdllm_dtype dtype, int B, int
  * the library runs on, held until the process ends.  The call allocates and
  * frees nothing.
  *   Sizes whose workspace exceeds FDLLM_STATIC_SCRATCH_BYTES are refused with
- *   FDLLM_ERR_SCRATCH (nothing enqueued).  Batches of 128 sequences or more
+ *   FDLLM_ERR_SCRATCH (nothing enqueued).  Batches of 256 sequences or more
  *   need no scratch at all; smaller ones need 12 B per position of the span
  *   (when tokens, conf or eps are not given) plus up to 384 B per position of
  *   blocks of at most 64 positions.

@@ -63,7 +63,7 @@
 #define FDLLM_TARGET_WAVES 16384  // small batches: split rows until about this many waves stream
 #endif
 #ifndef FDLLM_FUSED_MIN_B
-#define FDLLM_FUSED_MIN_B 128     // batches from this size run one workgroup per sequence
+#define FDLLM_FUSED_MIN_B 256     // batches from this size run one workgroup per sequence
 #endif
 #ifndef FDLLM_WAVES_PER_EU
 #define FDLLM_WAVES_PER_EU 0   // minimum waves per SIMD the fused kernel is compiled for (0: no hint)
@@ -159,9 +159,10 @@ __device__ __forceinline__ WavePartial row_pass(const typename Vec::Raw* __restr
 
   float m = kNegInf;
   float K = kRefFloor;
-  double acc[kAcc];
-#pragma unroll
-  for (int a = 0; a < kAcc; ++a) acc[a] = 0.0;
+  // acc: the terms of every batch but the kept one (below); pend: the kept
+  // batch's terms, dropped at the end, where the kept batch is summed again
+  // without one element equal to m (so no sum ever holds the lane maximum)
+  double acc = 0.0, pend = 0.0;
   // the batch in which this lane's maximum first appeared, and its vectors:
   // the lowest index of the row maximum is found in registers at the end
   // (a re-read from memory would cost a dependent HBM latency per row)
@@ -179,21 +180,29 @@ __device__ __forceinline__ WavePartial row_pass(const typename Vec::Raw* __restr
     for (int u = 0; u < U; ++u)
 #pragma unroll
       for (int e = 0; e < E; ++e) bm = fmaxf(bm, x[u][e]);
-    rec = bm > m ? batch : rec;
+    const bool grows = bm > m;
+    rec = grows ? batch : rec;
 #pragma unroll
-    for (int u = 0; u < U; ++u) keep[u] = bm > m ? r[u] : keep[u];
+    for (int u = 0; u < U; ++u) keep[u] = grows ? r[u] : keep[u];
     const float mn = fmaxf(m, bm);
     // a lane that has only seen padding keeps a finite reference, so that
     // padding terms are exp2(-inf) = 0 rather than exp2(-inf + inf)
     const float Kn = fmaxf(exp_ref(mn), kRefFloor);
-#pragma unroll
-    for (int a = 0; a < kAcc; ++a) acc[a] = rescale(acc[a], K, Kn);
+    acc = rescale(acc, K, Kn);
+    pend = rescale(pend, K, Kn);
     m = mn;
     K = Kn;
+    double t[kAcc];
+#pragma unroll
+    for (int a = 0; a < kAcc; ++a) t[a] = 0.0;
 #pragma unroll
     for (int u = 0; u < U; ++u)
 #pragma unroll
-      for (int e = 0; e < E; ++e) acc[(u * E + e) % kAcc] += (double)term(x[u][e], K);
+      for (int e = 0; e < E; ++e) t[(u * E + e) % kAcc] += (double)term(x[u][e], K);
+    const double bs = (t[0] + t[1]) + (t[2] + t[3]);
+    // a new kept batch sends the previous one's terms to acc
+    acc += grows ? pend : bs;
+    pend = grows ? bs : pend;
   };
 
   // Batches of U wave-loads; the first nbf are whole (no lane past the row
@@ -240,11 +249,45 @@ __device__ __forceinline__ WavePartial row_pass(const typename Vec::Raw* __restr
     consume(ra, jb);
   }
 
-  // combine the lane accumulators (fixed order)
-  double s = (acc[0] + acc[1]) + (acc[2] + acc[3]);
+  // the kept batch again, without one element equal to the lane maximum
+  // (padding is -inf: its terms are 0)
+  double s = acc;
+  if (rec >= 0) {
+    bool left_out = false;
+    double t[kAcc];
+#pragma unroll
+    for (int a = 0; a < kAcc; ++a) t[a] = 0.0;
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      float x[E];
+      Vec::unpack(keep[u], x);
+#pragma unroll
+      for (int e = 0; e < E; ++e) {
+        const bool skip = !left_out && x[e] == m;
+        left_out = left_out || skip;
+        t[(u * E + e) % kAcc] += skip ? 0.0 : (double)term(x[e], K);
+      }
+    }
+    s += (t[0] + t[1]) + (t[2] + t[3]);
+  }
 
   WavePartial out;
-  out.m = wave_max(m);
+  // (m, K, S) across lanes: fixed butterfly, bitwise equal in every lane
+  float mw = m;
+  mx_step<0>(mw, K, s);
+  mx_step<1>(mw, K, s);
+  mx_step<2>(mw, K, s);
+  mx_step<3>(mw, K, s);
+  mx_step<4>(mw, K, s);
+  {
+    float m0 = readlane_f32(mw, 0), m1 = readlane_f32(mw, 32);
+    float K0 = readlane_f32(K, 0), K1 = readlane_f32(K, 32);
+    double S0 = readlane_f64(s, 0), S1 = readlane_f64(s, 32);
+    mx_combine(m0, K0, S0, m1, K1, S1);
+    out.m = m0;
+    out.K = K0;
+    out.S = S0;
+  }
   // lowest index of the maximum: lanes holding it scan their kept batch
   int first = 0x7fffffff;
   if (m == out.m && rec >= 0) {
@@ -262,19 +305,6 @@ __device__ __forceinline__ WavePartial row_pass(const typename Vec::Raw* __restr
     }
   }
   out.first = wave_min(first);
-  // (K, S) across lanes
-  ks_step<0>(K, s);
-  ks_step<1>(K, s);
-  ks_step<2>(K, s);
-  ks_step<3>(K, s);
-  ks_step<4>(K, s);
-  {
-    float K0 = readlane_f32(K, 0), K1 = readlane_f32(K, 32);
-    double S0 = readlane_f64(s, 0), S1 = readlane_f64(s, 32);
-    ks_combine(K0, S0, K1, S1);
-    out.K = K0;
-    out.S = S0;
-  }
   return out;
 }
 
@@ -288,23 +318,54 @@ struct SplitShape {
   static constexpr int kThreads = kWaves * kWave;
 };
 
-// A row's S wave partials combined in part order; every plan that splits a
-// row S ways goes through this, so they all give the same bits.
+// A row's S wave partials merged by a fixed binary tree -- pairs (0,1),
+// (2,3), ..., then pairs of pairs, and so on -- in one of two forms that give
+// the same bits (mx_combine is bitwise commutative): a wavefront whose lanes
+// q < S hold part q (a butterfly over the lanes: every plan that streams a
+// row's parts within one workgroup), and one thread holding all S parts (the
+// selection kernels reading parts from the workspace).  The tree keeps the
+// dependent chain to log2 S merges and issues every part's load at once.
+template <int S>
+__device__ __forceinline__ RowResult combine_parts_lanes(const WavePartial& mine) {
+  float m = mine.m, K = mine.K;
+  double Sx = mine.S;
+  if constexpr (S >= 2) mx_step<0>(m, K, Sx);
+  if constexpr (S >= 4) mx_step<1>(m, K, Sx);
+  if constexpr (S >= 8) mx_step<2>(m, K, Sx);
+  if constexpr (S >= 16) mx_step<3>(m, K, Sx);
+  int f = mine.m == m ? mine.first : 0x7fffffff;   // lowest index among the parts holding M
+  if constexpr (S >= 2) f = min(f, partner_i32<0>(f));
+  if constexpr (S >= 4) f = min(f, partner_i32<1>(f));
+  if constexpr (S >= 8) f = min(f, partner_i32<2>(f));
+  if constexpr (S >= 16) f = min(f, partner_i32<3>(f));
+  return finish_row_x(m, K, Sx, f);
+}
+
 template <int S>
 __device__ __forceinline__ RowResult combine_parts(const WavePartial* part) {
-  float M = part[0].m;
-#pragma unroll
-  for (int q = 1; q < S; ++q) M = fmaxf(M, part[q].m);
-  const float K = exp_ref(M);
-  double Ssum = 0.0;
-  int first = 0x7fffffff;
+  float m[S], K[S];
+  double Sx[S];
+  int f[S];
 #pragma unroll
   for (int q = 0; q < S; ++q) {
-    const WavePartial pq = part[q];
-    Ssum += rescale(pq.S, pq.K, K);
-    if (pq.m == M) first = min(first, pq.first);
+    const WavePartial p = part[q];
+    m[q] = p.m;
+    K[q] = p.K;
+    Sx[q] = p.S;
+    f[q] = p.first;
   }
-  return finish_row(M, K, Ssum, first);
+  float mq[S];
+#pragma unroll
+  for (int q = 0; q < S; ++q) mq[q] = m[q];
+#pragma unroll
+  for (int width = 1; width < S; width <<= 1)
+#pragma unroll
+    for (int q = 0; q < S; q += 2 * width) mx_combine(m[q], K[q], Sx[q], m[q + width], K[q + width], Sx[q + width]);
+  int first = 0x7fffffff;
+#pragma unroll
+  for (int q = 0; q < S; ++q)
+    if (mq[q] == m[0]) first = min(first, f[q]);
+  return finish_row_x(m[0], K[0], Sx[0], first);
 }
 
 // Row group r of the grid handles the window-relative slot (b, q), q < W =
@@ -353,16 +414,21 @@ k_confidence(const typename Vec::Raw* __restrict__ logits, int B, int L, int nve
     if constexpr (S > 1) {
       if (lane == 0) part[wave] = wp;
       __syncthreads();
-    }
-    if (w == 0 && lane == 0 && inwin) {
+      if (w == 0 && cand) {
+        // the row group's first wave merges the S parts across its lanes
+        const WavePartial mine = lane < S ? part[rloc * S + lane]
+                                          : WavePartial{kNegInf, kRefFloor, 0.0, 0x7fffffff};
+        const RowResult rr = combine_parts_lanes<S>(mine);
+        if (lane == 0) store_row(out, slot, rr);
+      }
+      if (w == 0 && lane == 0 && inwin && !cand) store_default(out, slot);
+      __syncthreads();   // part[] is written again by the next trip
+    } else if (lane == 0 && inwin) {
       if (!cand)
         store_default(out, slot);
-      else if constexpr (S > 1)
-        store_row(out, slot, combine_parts<S>(&part[rloc * S]));
       else
-        store_row(out, slot, finish_row(wp.m, wp.K, wp.S, wp.first));
+        store_row(out, slot, finish_row_x(wp.m, wp.K, wp.S, wp.first));
     }
-    if constexpr (S > 1) __syncthreads();   // part[] is written again by the next trip
   }
 }
 
@@ -764,7 +830,7 @@ k_fused(const typename Vec::Raw* __restrict__ logits, int B, int L, int nvec,
     const int slot = s_cand[c];
     const size_t r = row0 + s + slot;
     const WavePartial wp = row_pass<Vec, U, 1>(logits + r * (size_t)nvec, nvec, 0);
-    const RowResult rr = finish_row(wp.m, wp.K, wp.S, wp.first);
+    const RowResult rr = finish_row_x(wp.m, wp.K, wp.S, wp.first);
     if (lane == 0) {
       store_row(out, r, rr);
       s_tok[slot] = rr.token;
@@ -835,7 +901,7 @@ k_fused_wide(const typename Vec::Raw* __restrict__ logits, int B, int L, int nve
     const int slot = s_cand[c];
     const size_t r = row0 + s + slot;
     const WavePartial wp = row_pass<Vec, U, 1>(logits + r * (size_t)nvec, nvec, 0);
-    const RowResult rr = finish_row(wp.m, wp.K, wp.S, wp.first);
+    const RowResult rr = finish_row_x(wp.m, wp.K, wp.S, wp.first);
     if (lane == 0) {
       store_row(out, r, rr);
       sh.tok[slot] = rr.token;

@@ -5,10 +5,12 @@ Bars (from the method's precision needs):
   * tokens, commit masks, n_commit, x, mask: bit-exact, except blocks the
     oracle flags as within 1e-6 of a decision boundary (reported);
   * conf and lse: relative error <= 1e-5 (lse relative to max(|lse|, 1));
-  * eps: relative error <= 1e-5, or absolute error <= EPS_ATOL = 2^-48: the
-    GPU forms s' = (S - e_M) / e_M from a double sum S that holds the greedy
-    term e_M (about 1) next to the others, so below eps ~ 1e-11 the double's
-    last bits (2^-53 of S per addition) dominate the relative error.
+  * eps: relative error <= 1e-5, or absolute error <= EPS_ATOL = 1e-30 (the
+    vocabulary pass sums every term but the greedy one, so eps keeps its
+    relative accuracy until the float32 terms underflow).  The LM-head folds
+    keep the greedy term e_M (about 1) in their double sum and form
+    s' = (S - e_M) / e_M, so below eps ~ 1e-11 the double's last bits set
+    the error there: EPS_ATOL_LMHEAD = 2^-48.
 """
 from __future__ import annotations
 
@@ -23,7 +25,8 @@ import oracle
 CONF_RTOL = 1e-5
 LSE_RTOL = 1e-5
 EPS_RTOL = 1e-5
-EPS_ATOL = 2.0 ** -48
+EPS_ATOL = 1e-30
+EPS_ATOL_LMHEAD = 2.0 ** -48
 MAX_BLOCK = 1024        # longest block the library accepts (FDLLM_MAX_BLOCK)
 
 

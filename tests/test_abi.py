@@ -217,7 +217,7 @@ def test_loop_entry_points_check_arguments(lib):
     for f in ("logits", "mask", "x", "block_start", "block_end"):
         setattr(d, f, 0x1000)
     assert lib.fdllm_generation_workspace_size(ctypes.byref(d), ctypes.byref(n)) == 0
-    assert n.value >= 3 * 4 * 64 * 4                 # B=4 < 128: decode scratch included
+    assert n.value >= 3 * 4 * 64 * 4                 # B=4 < 256: decode scratch included
     h = ctypes.c_void_p(0)
     assert lib.fdllm_generation_create(ctypes.byref(d), ctypes.byref(h)) == fd.ERR_WORKSPACE
     assert not h.value
@@ -278,6 +278,9 @@ def test_workspace_sizes_follow_the_plans(lib):
     assert small >= 3 * 32 * 4 + 32 * 16 * 24
     # a long span (L > 64) keeps single-workgroup rows: outputs only
     assert _ws(lib.fdllm_workspace_size, 8, 256, V, 0) < 3 * 8 * 256 * 4 + 1024 * 3
+    # one workgroup per sequence (no workspace) from 256 sequences on
+    assert _ws(lib.fdllm_workspace_size, 255, 32, V, 0) >= 3 * 255 * 32 * 4
+    assert _ws(lib.fdllm_workspace_size, 256, 32, V, 0) == 0
     # LM head: up to 32 positions need no partial logits
     s32 = _ws(lib.fdllm_lmhead_workspace_size, 1, 32, 4096, V)
     assert s32 < 4 << 20

@@ -42,7 +42,7 @@ OFFSETS = [
 
 
 @pytest.mark.parametrize("dt,offset", OFFSETS)
-@pytest.mark.parametrize("B,L,V", [(4, 32, 126464), (130, 8, 5000)])
+@pytest.mark.parametrize("B,L,V", [(4, 32, 126464), (130, 8, 5000), (260, 8, 5000)])
 def test_large_offset_parity(gpu, oracle_pool, dt, offset, B, L, V):
     say(f"[offset] B={B} L={L} V={V} {dt} offset {offset:g}")
     inp = _shifted(B, L, V, dt, offset, seed=int(abs(offset)) % 97 + B)

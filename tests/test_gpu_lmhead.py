@@ -18,7 +18,7 @@ import torch
 import oracle
 import workloads
 from parity import (say, candidates, compare_rows, check_defaults, compare_selection, CONF_RTOL,
-                    EPS_ATOL)
+                    EPS_ATOL_LMHEAD)
 
 pytestmark = pytest.mark.gpu
 
@@ -110,7 +110,7 @@ def test_lmhead_confidence_vs_oracle(gpu, B, L, d, V, kind, window):
             tol_l = delta + CONF_RTOL * max(abs(lse), 1.0)
         rc = abs(float(g[1][b, i]) - c) / c
         de = abs(float(g[2][b, i]) - ep)
-        re_ = de / max(ep, 1e-30) if de > EPS_ATOL else 0.0
+        re_ = de / max(ep, 1e-30) if de > EPS_ATOL_LMHEAD else 0.0
         rl = abs(float(g[3][b, i]) - lse)
         assert rc <= tol_c and re_ <= max(tol_e, 1e-5) and rl <= tol_l, (b, i, rc, re_, rl, tol_c)
         worst["conf"] = max(worst["conf"], rc)

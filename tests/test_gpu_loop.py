@@ -121,7 +121,7 @@ def test_generation_eta_tensor_vs_oracle(gpu):
     gen.close()
 
 
-@pytest.mark.parametrize("B,G,blk,V", [(8, 256, 32, 126464), (130, 64, 16, 512)])
+@pytest.mark.parametrize("B,G,blk,V", [(8, 256, 32, 126464), (130, 64, 16, 512), (260, 64, 16, 512)])
 def test_generation_graph_equals_eager(gpu, B, G, blk, V):
     """Graph replay in chunks, direct launches with a host check every step,
     and a second run of the same object all give the same generation."""

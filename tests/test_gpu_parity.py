@@ -44,9 +44,12 @@ SMALL = [
     (3, 33, 126464, torch.bfloat16, 33),
     (2, 17, 126464, torch.float32, 17),
     (2, 64, 6000, torch.float32, 64),
-    (130, 8, 520, torch.bfloat16, None),      # enough sequences for the fused plan
+    (130, 8, 520, torch.bfloat16, None),      # below 256 sequences: split plan
+    (260, 8, 520, torch.bfloat16, None),      # enough sequences for the fused plan
     (160, 12, 1024, torch.float32, 12),
-    (129, 3, 7, torch.bfloat16, None),        # fused plan, scalar path
+    (320, 12, 1024, torch.float32, 12),
+    (129, 3, 7, torch.bfloat16, None),        # split plan, scalar path
+    (257, 3, 7, torch.bfloat16, None),        # fused plan, scalar path
     (2, 24, 40000, torch.bfloat16, 24),       # rows split 8 ways (decode: two workgroups per row)
     (1, 20, 70001, torch.bfloat16, None),     # split 16 ways, scalar path
 ]
@@ -55,9 +58,10 @@ SMALL = [
 WIDE = [
     (3, 200, 1000, torch.bfloat16, 200),      # two-kernel plan
     (2, 1024, 300, torch.float32, 1024),      # largest block
-    (130, 100, 64, torch.bfloat16, 100),      # fused plan
-    (129, 700, 40, torch.bfloat16, 700),
-    (128, 1024, 13, torch.float32, 1024),     # fused plan, scalar path, largest block
+    (260, 100, 64, torch.bfloat16, 100),      # fused plan
+    (129, 700, 40, torch.bfloat16, 700),      # split plan
+    (257, 700, 40, torch.bfloat16, 700),
+    (256, 1024, 13, torch.float32, 1024),     # fused plan, scalar path, largest block
 ]
 
 
@@ -181,7 +185,7 @@ def test_crafted_profiles_on_gpu(gpu):
 
 def test_invalid_bounds_on_device(gpu):
     V = 64
-    for (BB, LL) in [(6, 20), (130, 100), (7, 1100), (130, 1030)]:
+    for (BB, LL) in [(6, 20), (130, 100), (260, 100), (7, 1100), (130, 1030), (260, 1030)]:
         case = workloads.random_case(BB, LL, V, torch.bfloat16, device="cuda", seed=7, poison=False)
         s = torch.zeros(BB, dtype=torch.int32); e = torch.zeros(BB, dtype=torch.int32)
         bounds = [(0, LL), (5, 4), (-1, 3), (0, LL + 1), (3, 3), (10, 10 + 65), (2, 2 + 1025)]
@@ -204,7 +208,7 @@ def test_invalid_bounds_on_device(gpu):
 
 
 def test_determinism_and_identical_rows(gpu):
-    B, L, V = 140, 16, 126464
+    B, L, V = 260, 16, 126464
     g = torch.Generator(device="cuda").manual_seed(5)
     one = torch.randn((1, 1, V), generator=g, device="cuda") * 2
     one[0, 0, 123] += 15.0
@@ -229,7 +233,7 @@ def test_determinism_and_identical_rows(gpu):
 
 REPEATED_MAX = [
     # (B, L, V, dtype): the row maximum repeats in many lanes and batches
-    (130, 3, 126464, torch.bfloat16),         # fused plan for the decode step
+    (260, 3, 126464, torch.bfloat16),         # fused plan for the decode step
     (2, 24, 40000, torch.bfloat16),           # rows split 8 ways
     (1, 20, 70001, torch.bfloat16),           # split 16 ways, scalar path
     (2, 9, 126464, torch.float32),
@@ -405,3 +409,37 @@ def test_decode_step_random_shapes(gpu, B, L, V, dt, window):
         assert np.array_equal(mask.cpu().numpy()[ok], r.mask[ok])
         for name, t in zip(("tokens", "conf", "eps", "lse"), ref_conf):
             assert torch.equal(o[name].view(torch.int32), t.view(torch.int32)), name
+
+
+@pytest.mark.parametrize("B,L,V,dt", [(3, 24, 5000, torch.float32), (2, 16, 126464, torch.bfloat16),
+                                      (260, 4, 3000, torch.bfloat16), (4, 9, 8191, torch.float32)])
+def test_very_confident_rows_eps(gpu, B, L, V, dt):
+    """Rows whose greedy token stands 22-85 above an N(0,1) background: eps
+    from ~1e-6 down to ~1e-32.  The pass never sums the greedy term, so eps
+    matches the oracle to 1e-5 relative down to the float32 terms' underflow."""
+    g = torch.Generator().manual_seed(B * 1000 + V)
+    rows = torch.randn((B * L, V), generator=g)
+    tok = torch.randint(0, V, (B * L,), generator=g)
+    h = 22.0 + 63.0 * torch.rand((B * L,), generator=g)
+    rows[torch.arange(B * L), tok] = h
+    logits = rows.view(B, L, V).to(dt).to("cuda")
+    mask = torch.ones((B, L), dtype=torch.uint8, device="cuda")
+    start = torch.zeros(B, dtype=torch.int32, device="cuda")
+    end = torch.full((B,), L, dtype=torch.int32, device="cuda")
+    inp = workloads.StepInputs(logits, mask, start, end, torch.full((B, L), -1, dtype=torch.int32,
+                                                                    device="cuda"), "very confident")
+    say(f"[very confident] B={B} L={L} V={V} {dt}")
+    gc = [t.cpu().numpy() for t in gpu_confidence(gpu, inp)]
+    o = oracle_confidence_subset(inp, range(B))
+    cells = candidates(mask.cpu().numpy(), start.cpu().numpy(), end.cpu().numpy(), range(B))
+    worst = compare_rows(*gc, *o, cells)
+    assert float(np.min(o[2][mask.cpu().numpy() != 0])) < 1e-25
+    # the decode step's pass gives the same bits
+    d = dict(tokens=torch.empty((B, L), dtype=torch.int32, device="cuda"),
+             conf=torch.empty((B, L), device="cuda"), eps=torch.empty((B, L), device="cuda"),
+             lse=torch.empty((B, L), device="cuda"))
+    gpu.fdllm_decode_step(logits, mask.clone(), start, end, inp.x.clone(), "profile", 1.0, **d)
+    torch.cuda.synchronize()
+    for k, t in zip(("tokens", "conf", "eps", "lse"), gc):
+        assert np.array_equal(d[k].cpu().numpy().view(np.int32), t.view(np.int32)), k
+    say(f"  worst {worst}")

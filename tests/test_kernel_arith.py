@@ -11,7 +11,8 @@ documented bound |logit| <= 1e7, that
 
   * the maximum's own argument lies in (-1, 0] (no overflow, no underflow);
   * the confidence and eps built from the emulated sums agree with the
-    oracle on the same rows.
+    oracle on the same rows, eps to 1e-5 relative also when it is tiny (the
+    greedy element's term never enters a sum).
 """
 import math
 
@@ -45,22 +46,38 @@ def arg(x, K) -> np.float32:
 
 
 def emulate_row(row: np.ndarray, batch: int = 32):
-    """(token, conf, eps) by the kernel's one-lane streaming scheme."""
+    """(token, conf, eps) by the kernel's one-lane streaming scheme: the terms
+    of every batch but the one where the running maximum first appeared go
+    to acc; that batch is summed again at the end without one element equal
+    to the maximum, so no sum ever holds the greedy term."""
     row = row.astype(np.float32)
-    m, K, S, first = -np.inf, np.float32(-3.0e38), 0.0, -1
+    m, K, acc, pend, first, kept = -np.inf, np.float32(-3.0e38), 0.0, 0.0, -1, None
     for b0 in range(0, row.size, batch):
         xs = row[b0:b0 + batch]
         bm = xs.max()
-        if bm > m:
-            first = b0 + int(np.argmax(xs))
-            Kn = max(exp_ref(bm), np.float32(-3.0e38))
-            S = math.ldexp(S, int(max(float(K) - float(Kn), -2000.0)))
-            m, K = bm, Kn
+        grows = bm > m
+        Kn = max(exp_ref(max(m, bm)), np.float32(-3.0e38))
+        shift = int(max(float(K) - float(Kn), -2000.0))
+        acc, pend = math.ldexp(acc, shift), math.ldexp(pend, shift)
+        m, K = max(m, bm), Kn
+        bs = 0.0
         for x in xs:
-            S += float(np.float32(np.exp2(np.float64(arg(x, K)))))
-    Kr = exp_ref(np.float32(m))
-    eM = math.ldexp(float(np.float32(np.exp2(np.float64(arg(m, Kr))))), int(float(Kr) - float(K)))
-    sp = max((S - eM) / eM, 0.0)
+            bs += float(np.float32(np.exp2(np.float64(arg(x, K)))))
+        if grows:
+            first = b0 + int(np.argmax(xs))
+            kept = xs
+            acc += pend
+            pend = bs
+        else:
+            acc += bs
+    left_out = False
+    for x in kept:
+        if not left_out and x == m:
+            left_out = True
+            continue
+        acc += float(np.float32(np.exp2(np.float64(arg(x, K)))))
+    eM = float(np.float32(np.exp2(np.float64(arg(m, exp_ref(np.float32(m)))))))
+    sp = acc / eM
     return first, 1.0 / (1.0 + sp), sp / (1.0 + sp)
 
 
@@ -110,3 +127,18 @@ def test_emulated_pass_matches_oracle(offset):
     assert t == ot
     assert abs(c - oc) <= 1e-5 * oc
     assert abs(e - oe) <= 1e-5 * oe
+
+
+@pytest.mark.parametrize("spike", [22.0, 35.0, 50.0, 65.0, 80.0])
+def test_emulated_eps_of_very_confident_rows(spike):
+    # eps ~ V e^(1/2 - spike): from 1e-6 down to ~1e-31; the greedy term never
+    # enters a sum, so eps keeps its relative accuracy
+    rng = np.random.default_rng(int(spike))
+    V = 4000
+    row = rng.normal(0.0, 1.0, V).astype(np.float32)
+    row[rng.integers(0, V)] = np.float32(spike)
+    t, c, e = emulate_row(row)
+    ot, oc, oe, _ = oracle.position_confidence(row.astype(np.float64))
+    assert t == ot
+    assert oe < 1e-5
+    assert abs(e - oe) <= 1e-5 * oe, (e, oe)
