@@ -431,6 +431,69 @@ def per_workload_markdown(rows, stress, stream_gbps, cmd) -> str:
     return "\n".join(out) + "\n"
 
 
+def plan_sweep(reps: int, md_path):
+    """Cold decode-step times over the batch size B and the masked rows per
+    block m (L = 32, V = 126464 bf16, profile f = 1): the plan the library
+    picks at each B (one workgroup per sequence from 256 sequences, rows split
+    over waves plus a selection launch below).  One JSON line; optionally a
+    markdown table."""
+    import torch
+    import paper_2606_02955_amd as fd
+    fd.load()
+    dev = torch.device("cuda", 0)
+    V, L = 126464, 32
+    Bs = (64, 96, 128, 160, 192, 224, 256, 320, 384, 512, 1024)
+    ms = (32, 16, 8, 4, 1)
+    g = torch.Generator(device=dev).manual_seed(5)
+    big = torch.empty((max(Bs), L, V), dtype=torch.bfloat16, device=dev)
+    for b0 in range(0, big.shape[0], 64):
+        big[b0:b0 + 64].normal_(generator=g)
+    scratch = torch.empty(512 << 20, dtype=torch.uint8, device=dev)
+    res = []
+    for B in Bs:
+        logits = big[:B]
+        start = torch.zeros(B, dtype=torch.int32, device=dev)
+        end = torch.full((B,), L, dtype=torch.int32, device=dev)
+        x0 = torch.full((B, L), -1, dtype=torch.int32, device=dev)
+        nc = torch.empty(B, dtype=torch.int32, device=dev)
+        for m in ms:
+            mask0 = torch.zeros((B, L), dtype=torch.uint8, device=dev)
+            mask0.scatter_(1, torch.rand((B, L), generator=g, device=dev).argsort(1)[:, :m], 1)
+            mask, x = mask0.clone(), x0.clone()
+            ws = fd.fdllm_decode_step(logits, mask, start, end, x, "profile", 1.0, n_commit=nc)
+            ts = []
+            for k in range(reps + 2):
+                mask.copy_(mask0)
+                x.copy_(x0)
+                scratch.fill_(k & 0x7F)            # evicts the logits from L2 and the Infinity Cache
+                e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                e0.record()
+                fd.fdllm_decode_step(logits, mask, start, end, x, "profile", 1.0, n_commit=nc, workspace=ws)
+                e1.record()
+                torch.cuda.synchronize()
+                if k >= 2:
+                    ts.append(e0.elapsed_time(e1) * 1e-3)
+            t = sorted(ts)[len(ts) // 2]
+            nbytes = B * m * V * 2
+            res.append({"B": B, "m": m, "us": t * 1e6, "GBps": nbytes / t / 1e9,
+                        "plan": "one workgroup per sequence" if B >= 256 else "rows split over waves + selection"})
+            log(f"plan sweep B={B} m={m}: {t * 1e6:.1f} us, {nbytes / t / 1e9:.0f} GB/s")
+    print(json.dumps({"metric": "decode-step time over batch size and masked rows per block (cold)",
+                      "L": L, "V": V, "dtype": "bf16", "reps": reps, "rows": res}), flush=True)
+    if md_path:
+        out = ["# Decode-step plan sweep (one MI355X)", "", "Command (from the repository root):", "",
+               f"    python bench.py --plan-sweep --plan-sweep-md <file>", "",
+               "Cold decode steps (512 MB overwritten before each), L = 32, V = 126464 bf16, profile f = 1, "
+               f"median of {reps}; m of the 32 positions of every block masked.  B >= 256 runs one workgroup "
+               "per sequence, smaller batches the split rows plus a selection launch.  Cells: µs (logits GB/s).", "",
+               "| B | " + " | ".join(f"m = {m}" for m in ms) + " |", "|---|" + "---|" * len(ms)]
+        for B in Bs:
+            cells = [r for r in res if r["B"] == B]
+            out.append(f"| {B} | " + " | ".join(f"{r['us']:.1f} ({r['GBps']:.0f})" for r in cells) + " |")
+        with open(md_path, "w") as fh:
+            fh.write("\n".join(out) + "\n")
+
+
 def lmhead_only(n, steps, warmup):
     """Times fdllm_lmhead_confidence on n positions (one sequence's block of
     up to 32, or n / 32 of them) with random bf16 hidden states and output
@@ -488,6 +551,9 @@ def main():
                          "warm-up steps, so the clocks are at their loaded steady state (0: none)")
     ap.add_argument("--copy-calibration-mb", type=int, default=1024,
                     help="size of a plain device copy timed (and counted by rocprofv3) for reference")
+    ap.add_argument("--plan-sweep", action="store_true",
+                    help="instead: cold decode-step times over batch size and masked rows per block")
+    ap.add_argument("--plan-sweep-md", default=None, help="write the plan sweep as a markdown table here")
     ap.add_argument("--lmhead-positions", type=int, default=0,
                     help="instead: time only the fused LM head on this many positions "
                          "(d=4096, V=126464 bf16; one JSON line)")
@@ -500,6 +566,9 @@ def main():
     param = args.param if args.param is not None else (0.9 if args.selector == "threshold" else 1.0)
     if args.lmhead_positions > 0:
         lmhead_only(args.lmhead_positions, args.steps, args.warmup)
+        return
+    if args.plan_sweep:
+        plan_sweep(10, args.plan_sweep_md)
         return
 
     pool, pool_note = None, None

@@ -272,22 +272,16 @@ __device__ __forceinline__ WavePartial row_pass(const typename Vec::Raw* __restr
   }
 
   WavePartial out;
-  // (m, K, S) across lanes: fixed butterfly, bitwise equal in every lane
-  float mw = m;
-  mx_step<0>(mw, K, s);
-  mx_step<1>(mw, K, s);
-  mx_step<2>(mw, K, s);
-  mx_step<3>(mw, K, s);
-  mx_step<4>(mw, K, s);
-  {
-    float m0 = readlane_f32(mw, 0), m1 = readlane_f32(mw, 32);
-    float K0 = readlane_f32(K, 0), K1 = readlane_f32(K, 32);
-    double S0 = readlane_f64(s, 0), S1 = readlane_f64(s, 32);
-    mx_combine(m0, K0, S0, m1, K1, S1);
-    out.m = m0;
-    out.K = K0;
-    out.S = S0;
-  }
+  // across lanes: the wave maximum M and its reference, then every lane but
+  // the lowest one holding M puts its own maximum's term back, and a fixed
+  // butterfly sums (bitwise equal in every lane)
+  out.m = wave_max(m);
+  out.K = fmaxf(exp_ref(out.m), kRefFloor);
+  const unsigned long long holders = __ballot(m == out.m);
+  const bool owner = lane == (int)__builtin_ctzll(holders);
+  double v = rescale(s, K, out.K);
+  if (!owner) v += rescale((double)term(m, K), K, out.K);
+  out.S = wave_sum_f64(v);
   // lowest index of the maximum: lanes holding it scan their kept batch
   int first = 0x7fffffff;
   if (m == out.m && rec >= 0) {
@@ -318,54 +312,68 @@ struct SplitShape {
   static constexpr int kThreads = kWaves * kWave;
 };
 
-// A row's S wave partials merged by a fixed binary tree -- pairs (0,1),
-// (2,3), ..., then pairs of pairs, and so on -- in one of two forms that give
-// the same bits (mx_combine is bitwise commutative): a wavefront whose lanes
-// q < S hold part q (a butterfly over the lanes: every plan that streams a
-// row's parts within one workgroup), and one thread holding all S parts (the
-// selection kernels reading parts from the workspace).  The tree keeps the
-// dependent chain to log2 S merges and issues every part's load at once.
+// A row's S wave partials combined: the row maximum M and its reference,
+// every part but the lowest-index one holding M puts its own maximum's term
+// back, and the parts' sums add up by a fixed binary tree -- pairs (0,1),
+// (2,3), ..., then pairs of pairs -- in one of two forms that give the same
+// bits: a wavefront whose lanes q < S hold part q (a butterfly over the
+// lanes, used where a row's parts meet in one workgroup) and one thread
+// holding all S parts (the selection kernels reading parts from the
+// workspace; every part's load is issued at once).
 template <int S>
 __device__ __forceinline__ RowResult combine_parts_lanes(const WavePartial& mine) {
-  float m = mine.m, K = mine.K;
-  double Sx = mine.S;
-  if constexpr (S >= 2) mx_step<0>(m, K, Sx);
-  if constexpr (S >= 4) mx_step<1>(m, K, Sx);
-  if constexpr (S >= 8) mx_step<2>(m, K, Sx);
-  if constexpr (S >= 16) mx_step<3>(m, K, Sx);
-  int f = mine.m == m ? mine.first : 0x7fffffff;   // lowest index among the parts holding M
+  const int lane = lane_id();
+  float M = mine.m;
+  if constexpr (S >= 2) M = fmaxf(M, partner_f32<0>(M));
+  if constexpr (S >= 4) M = fmaxf(M, partner_f32<1>(M));
+  if constexpr (S >= 8) M = fmaxf(M, partner_f32<2>(M));
+  if constexpr (S >= 16) M = fmaxf(M, partner_f32<3>(M));
+  const float K = fmaxf(exp_ref(M), kRefFloor);
+  const unsigned long long group = (S >= 64 ? ~0ull : ((1ull << S) - 1ull)) << (lane / S * S);
+  const unsigned long long holders = __ballot(mine.m == M) & group;
+  const bool owner = lane == (int)__builtin_ctzll(holders);
+  double v = rescale(mine.S, mine.K, K);
+  if (!owner) v += rescale((double)term(mine.m, mine.K), mine.K, K);
+  if constexpr (S >= 2) v += partner_f64<0>(v);
+  if constexpr (S >= 4) v += partner_f64<1>(v);
+  if constexpr (S >= 8) v += partner_f64<2>(v);
+  if constexpr (S >= 16) v += partner_f64<3>(v);
+  int f = mine.m == M ? mine.first : 0x7fffffff;   // lowest index among the parts holding M
   if constexpr (S >= 2) f = min(f, partner_i32<0>(f));
   if constexpr (S >= 4) f = min(f, partner_i32<1>(f));
   if constexpr (S >= 8) f = min(f, partner_i32<2>(f));
   if constexpr (S >= 16) f = min(f, partner_i32<3>(f));
-  return finish_row_x(m, K, Sx, f);
+  return finish_row_x(M, K, v, f);
 }
 
 template <int S>
 __device__ __forceinline__ RowResult combine_parts(const WavePartial* part) {
-  float m[S], K[S];
-  double Sx[S];
-  int f[S];
+  WavePartial p[S];
+#pragma unroll
+  for (int q = 0; q < S; ++q) p[q] = part[q];
+  float M = p[0].m;
+#pragma unroll
+  for (int q = 1; q < S; ++q) M = fmaxf(M, p[q].m);
+  const float K = fmaxf(exp_ref(M), kRefFloor);
+  int owner = S;
+#pragma unroll
+  for (int q = S - 1; q >= 0; --q)
+    if (p[q].m == M) owner = q;
+  double v[S];
 #pragma unroll
   for (int q = 0; q < S; ++q) {
-    const WavePartial p = part[q];
-    m[q] = p.m;
-    K[q] = p.K;
-    Sx[q] = p.S;
-    f[q] = p.first;
+    v[q] = rescale(p[q].S, p[q].K, K);
+    if (q != owner) v[q] += rescale((double)term(p[q].m, p[q].K), p[q].K, K);
   }
-  float mq[S];
-#pragma unroll
-  for (int q = 0; q < S; ++q) mq[q] = m[q];
 #pragma unroll
   for (int width = 1; width < S; width <<= 1)
 #pragma unroll
-    for (int q = 0; q < S; q += 2 * width) mx_combine(m[q], K[q], Sx[q], m[q + width], K[q + width], Sx[q + width]);
+    for (int q = 0; q < S; q += 2 * width) v[q] += v[q + width];
   int first = 0x7fffffff;
 #pragma unroll
   for (int q = 0; q < S; ++q)
-    if (mq[q] == m[0]) first = min(first, f[q]);
-  return finish_row_x(m[0], K[0], Sx[0], first);
+    if (p[q].m == M) first = min(first, p[q].first);
+  return finish_row_x(M, K, v[0], first);
 }
 
 // Row group r of the grid handles the window-relative slot (b, q), q < W =

@@ -134,32 +134,23 @@ __device__ __forceinline__ void ks_step(float& K, double& S) {
   ks_combine(K, S, K2, S2);
 }
 
-// The vocabulary pass keeps, for every stretch of a row, the sum of the terms
-// of all its elements except one occurrence of the stretch's maximum m.
-// Merging two stretches puts the smaller maximum's term back (the larger
-// stays out; on a tie either, as both terms are equal), so the whole row's
-// sum is s' e_M = sum over every element but one occurrence of the row
-// maximum, built without the greedy term and without any subtraction: eps
-// keeps its relative accuracy however close c is to 1.  Bitwise symmetric,
-// so butterfly partners end with identical values.
-__device__ __forceinline__ void mx_combine(float& m, float& K, double& S, float m2, float K2,
-                                           double S2) {
-  const bool other_lower = m2 <= m;
-  const float ml = other_lower ? m2 : m;    // the maximum that re-enters the sum
-  const float Kl = other_lower ? K2 : K;
-  const float Kn = fmaxf(K, K2);
-  const double back = rescale((double)term(ml, Kl), Kl, Kn);
-  S = (rescale(S, K, Kn) + rescale(S2, K2, Kn)) + back;
-  K = Kn;
-  m = fmaxf(m, m2);
-}
+// The vocabulary pass keeps, for every stretch of a row (a lane's elements,
+// a wave's, a part of a split row), the sum of the terms of all its elements
+// except one occurrence of the stretch's maximum m.  Stretches are combined
+// by taking the largest maximum M, having every stretch but the lowest-index
+// one that holds M put its own maximum's term back, and adding in a fixed
+// order: the row's sum is then every term but one occurrence of the row
+// maximum, s' e_M, built without the greedy term and without any
+// subtraction, so eps keeps its relative accuracy however close c is to 1.
 
-template <int Step>
-__device__ __forceinline__ void mx_step(float& m, float& K, double& S) {
-  const float m2 = partner_f32<Step>(m);
-  const float K2 = partner_f32<Step>(K);
-  const double S2 = partner_f64<Step>(S);
-  mx_combine(m, K, S, m2, K2, S2);
+// Sum over the wave by a fixed butterfly; every lane ends with the same bits.
+__device__ __forceinline__ double wave_sum_f64(double v) {
+  v += partner_f64<0>(v);
+  v += partner_f64<1>(v);
+  v += partner_f64<2>(v);
+  v += partner_f64<3>(v);
+  v += partner_f64<4>(v);
+  return readlane_f64(v, 0) + readlane_f64(v, 32);
 }
 
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
@@ -171,7 +162,7 @@ struct WavePartial {
   float m;    // maximum over the wave's elements (uniform)
   float K;    // exp_ref(m) (uniform)
   double S;   // sum of 2^(x log2e - K) over the wave's elements (uniform); the
-              // vocabulary pass leaves one occurrence of m out (mx_combine),
+              // vocabulary pass leaves one occurrence of m out,
               // the LM-head folds keep every term (finish_row)
   int first;  // lowest element index holding m (uniform)
 };
@@ -182,7 +173,7 @@ struct RowResult {
 };
 
 // Final step of a row of the vocabulary pass from its (M, K, S, first), S
-// without the greedy element's term (see mx_combine): s' = S / e_M.
+// without the greedy element's term: s' = S / e_M.
 __device__ __forceinline__ RowResult finish_row_x(float M, float K, double S, int first) {
   const float Kr = exp_ref(M);
   const double eM = rescale((double)term(M, Kr), Kr, K);

@@ -22,5 +22,5 @@ def test_help_lists_the_contract_flags():
     r = _bench("--help")
     assert r.returncode == 0
     for flag in ("--gpus", "--steps", "--warmup", "--settle-ms", "--per-workload",
-                 "--lmhead-positions", "--no-cpu-baseline"):
+                 "--lmhead-positions", "--no-cpu-baseline", "--plan-sweep"):
         assert flag in r.stdout, flag

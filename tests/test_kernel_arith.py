@@ -12,7 +12,10 @@ documented bound |logit| <= 1e7, that
   * the maximum's own argument lies in (-1, 0] (no overflow, no underflow);
   * the confidence and eps built from the emulated sums agree with the
     oracle on the same rows, eps to 1e-5 relative also when it is tiny (the
-    greedy element's term never enters a sum).
+    greedy element's term never enters a sum);
+  * the merge of lanes and of a row's parts leaves out exactly one
+    occurrence of the row maximum however the maximum is spread over them
+    (ties within a lane, across lanes and across parts).
 """
 import math
 
@@ -45,40 +48,97 @@ def arg(x, K) -> np.float32:
     return np.float32(float(x) * float(LOG2E_F) - float(K))
 
 
-def emulate_row(row: np.ndarray, batch: int = 32):
-    """(token, conf, eps) by the kernel's one-lane streaming scheme: the terms
-    of every batch but the one where the running maximum first appeared go
-    to acc; that batch is summed again at the end without one element equal
-    to the maximum, so no sum ever holds the greedy term."""
-    row = row.astype(np.float32)
-    m, K, acc, pend, first, kept = -np.inf, np.float32(-3.0e38), 0.0, 0.0, -1, None
-    for b0 in range(0, row.size, batch):
-        xs = row[b0:b0 + batch]
-        bm = xs.max()
+def term(x, K) -> float:
+    """The float32 exp2 of the fused argument, widened to double."""
+    return float(np.float32(np.exp2(np.float64(arg(x, K)))))
+
+
+def rescale(s: float, a, b) -> float:
+    """s * 2^(a - b) for integer-valued a <= b (exact, as ldexp)."""
+    return math.ldexp(s, int(max(float(a) - float(b), -2000.0)))
+
+
+def ref_of(m) -> np.float32:
+    """The reference with the floor a stretch of padding only keeps."""
+    if m == -np.inf:
+        return np.float32(-3.0e38)
+    return max(exp_ref(np.float32(m)), np.float32(-3.0e38))
+
+
+def emulate_stretch(xs: np.ndarray, idx: np.ndarray, batch: int):
+    """(m, K, s, first) of one stretch by the kernel's one-lane streaming
+    scheme: the terms of every batch but the one where the running maximum
+    first appeared go to acc; that batch is summed again at the end without
+    one element equal to the maximum, so s holds every term of the stretch
+    but one occurrence of m."""
+    m, K, acc, pend, first, kept = -np.inf, np.float32(-3.0e38), 0.0, 0.0, 0x7FFFFFFF, None
+    for b0 in range(0, xs.size, batch):
+        xb = xs[b0:b0 + batch]
+        bm = xb.max()
         grows = bm > m
-        Kn = max(exp_ref(max(m, bm)), np.float32(-3.0e38))
-        shift = int(max(float(K) - float(Kn), -2000.0))
-        acc, pend = math.ldexp(acc, shift), math.ldexp(pend, shift)
+        Kn = ref_of(max(m, bm))
+        acc, pend = rescale(acc, K, Kn), rescale(pend, K, Kn)
         m, K = max(m, bm), Kn
-        bs = 0.0
-        for x in xs:
-            bs += float(np.float32(np.exp2(np.float64(arg(x, K)))))
+        bs = sum(term(x, K) for x in xb)
         if grows:
-            first = b0 + int(np.argmax(xs))
-            kept = xs
+            first = int(idx[b0 + int(np.argmax(xb))])
+            kept = xb
             acc += pend
             pend = bs
         else:
             acc += bs
-    left_out = False
-    for x in kept:
-        if not left_out and x == m:
-            left_out = True
-            continue
-        acc += float(np.float32(np.exp2(np.float64(arg(x, K)))))
-    eM = float(np.float32(np.exp2(np.float64(arg(m, exp_ref(np.float32(m)))))))
-    sp = acc / eM
+    if kept is not None:
+        left_out = False
+        for x in kept:
+            if not left_out and x == m:
+                left_out = True
+                continue
+            acc += term(x, K)
+    return m, K, acc, first
+
+
+def combine(parts):
+    """Stretches merged as the kernel merges lanes and a row's parts: the
+    largest maximum M, every stretch but the lowest-index one holding M puts
+    its own maximum's term back, then one sum."""
+    M = max(p[0] for p in parts)
+    K = ref_of(M)
+    owner = next(i for i, p in enumerate(parts) if p[0] == M)
+    total = 0.0
+    for i, (m, Km, s, _) in enumerate(parts):
+        total += rescale(s, Km, K)
+        if i != owner:
+            total += rescale(term(m, Km), Km, K)
+    return M, K, total, min(p[3] for p in parts if p[0] == M)
+
+
+def finish(M, K, S, first):
+    """(token, conf, eps) from a row's (M, K, S): S / e_M is the sum of the
+    other terms over the greedy one."""
+    Kr = exp_ref(np.float32(M))
+    sp = S / rescale(term(M, Kr), Kr, K)
     return first, 1.0 / (1.0 + sp), sp / (1.0 + sp)
+
+
+def emulate_row(row: np.ndarray, E: int = 8, U: int = 4, lanes: int = 1, parts: int = 1):
+    """(token, conf, eps) of one row the kernel's way: vectors of E elements,
+    wave-load j of part w covering vectors (w + j parts) lanes + l for lanes
+    l, each lane streaming batches of U vectors, lanes merged into a wave
+    partial, the row's parts merged last."""
+    row = row.astype(np.float32)
+    nvec = (row.size + E - 1) // E
+    waves = []
+    for w in range(parts):
+        lane_parts = []
+        for lane in range(lanes):
+            vecs = [v for v in range(w * lanes + lane, nvec, parts * lanes)]
+            idx = np.array([v * E + e for v in vecs for e in range(E) if v * E + e < row.size],
+                           dtype=np.int64)
+            xs = row[idx] if idx.size else np.zeros(0, np.float32)
+            lane_parts.append(emulate_stretch(xs, idx, U * E) if idx.size
+                              else (-np.inf, np.float32(-3.0e38), 0.0, 0x7FFFFFFF))
+        waves.append(combine(lane_parts))
+    return finish(*combine(waves))
 
 
 MAGNITUDES = [1e3, 1e4, 1e5, 1e6, 3e6, 9.99e6, MAX_ABS_LOGIT]
@@ -142,3 +202,43 @@ def test_emulated_eps_of_very_confident_rows(spike):
     assert t == ot
     assert oe < 1e-5
     assert abs(e - oe) <= 1e-5 * oe, (e, oe)
+
+
+@pytest.mark.parametrize("lanes,parts", [(1, 1), (4, 1), (64, 1), (8, 4), (64, 16)])
+@pytest.mark.parametrize("spike", [0.0, 30.0])
+def test_emulated_split_rows_match_oracle(lanes, parts, spike):
+    rng = np.random.default_rng(lanes * 100 + parts)
+    V = 5003                       # ragged: the last vector is partial
+    row = rng.normal(0.0, 1.0, V).astype(np.float32)
+    if spike:
+        row[rng.integers(0, V)] = np.float32(spike)
+    t, c, e = emulate_row(row, lanes=lanes, parts=parts)
+    ot, oc, oe, _ = oracle.position_confidence(row.astype(np.float64))
+    assert t == ot
+    assert abs(c - oc) <= 1e-5 * oc
+    assert abs(e - oe) <= 1e-5 * oe, (e, oe)
+
+
+@pytest.mark.parametrize("where", ["one_lane", "across_lanes", "across_parts", "everywhere"])
+def test_emulated_tied_maxima(where):
+    # k copies of the maximum: the greedy token is the lowest index and
+    # s' counts the k - 1 other copies, so eps >= (k - 1) / k
+    rng = np.random.default_rng(len(where))
+    V, E, lanes, parts = 4096, 8, 8, 4
+    row = rng.normal(0.0, 1.0, V).astype(np.float32)
+    top = np.float32(12.0)
+    if where == "one_lane":
+        pos = [3, 5, 3 + E * lanes * parts]          # lane 0 of part 0, two batches
+    elif where == "across_lanes":
+        pos = [E * 1 + 2, E * 5, E * 7 + 7]         # lanes 1, 5, 7 of part 0
+    elif where == "across_parts":
+        pos = [E * lanes * 1, E * lanes * 2 + 9, E * lanes * 3 + 1]
+    else:
+        pos = list(rng.choice(V, 40, replace=False))
+    row[pos] = top
+    t, c, e = emulate_row(row, E=E, U=2, lanes=lanes, parts=parts)
+    ot, oc, oe, _ = oracle.position_confidence(row.astype(np.float64))
+    assert t == ot == min(pos)
+    assert e >= (len(pos) - 1) / len(pos) * (1 - 1e-6)
+    assert abs(c - oc) <= 1e-5 * oc
+    assert abs(e - oe) <= 1e-5 * oe
