@@ -73,6 +73,49 @@ def measured_traffic():
     return t.get("hbm_bytes_per_launch")
 
 
+def _counter_means(csv_path: str, counter: str):
+    """Mean value per dispatch of `counter` for the calibration kernel (the
+    elementwise add of the uint8 copy reference) and the fused decode step,
+    from a rocprofv3 counter_collection csv."""
+    import csv
+    sums = {"copy": [0.0, 0], "fused": [0.0, 0]}
+    with open(csv_path) as fh:
+        for row in csv.DictReader(fh):
+            if row.get("Counter_Name") != counter:
+                continue
+            name = row.get("Kernel_Name", "")
+            # the calibration is torch.add(uint8 tensor, 1): its functor names the dtype
+            key = "fused" if "k_fused<" in name else "copy" if "add<unsigned char>" in name else None
+            if key:
+                sums[key][0] += float(row["Counter_Value"])
+                sums[key][1] += 1
+    if not sums["copy"][1] or not sums["fused"][1]:
+        raise SystemExit(f"{csv_path}: no {counter} rows for the elementwise add and k_fused")
+    return {k: v[0] / v[1] for k, v in sums.items()}, {k: v[1] for k, v in sums.items()}
+
+
+def traffic_from(fetch_csv: str, write_csv: str, out_path: str, copy_mb: int):
+    """HBM bytes per fused-step launch from the FETCH_SIZE and WRITE_SIZE runs
+    (KiB per dispatch), each scaled by what the counter reads for the
+    elementwise add of copy_mb MiB (which reads and writes exactly that)."""
+    n = copy_mb << 20
+    f, fc = _counter_means(fetch_csv, "FETCH_SIZE")
+    w, wc = _counter_means(write_csv, "WRITE_SIZE")
+    fetch_scale = n / (f["copy"] * 1024.0)
+    write_scale = n / (w["copy"] * 1024.0)
+    t = {"kernel": "k_fused (stress_b1024_l32 decode step)",
+         "workload": "throughput stress B=1024 L=32 V=126464 bf16",
+         "source_sha256_16": source_digest(),
+         "fetch_kib_per_dispatch": f["fused"], "write_kib_per_dispatch": w["fused"],
+         "dispatches": {"fetch": fc, "write": wc},
+         "fetch_scale": fetch_scale, "write_scale": write_scale,
+         "hbm_bytes_per_launch": (f["fused"] * fetch_scale + w["fused"] * write_scale) * 1024.0}
+    with open(out_path, "w") as fh:
+        json.dump(t, fh, indent=1)
+        fh.write("\n")
+    print(json.dumps(t))
+
+
 def cpu_model() -> str:
     try:
         for line in open("/proc/cpuinfo"):
@@ -557,7 +600,16 @@ def main():
     ap.add_argument("--lmhead-positions", type=int, default=0,
                     help="instead: time only the fused LM head on this many positions "
                          "(d=4096, V=126464 bf16; one JSON line)")
+    ap.add_argument("--traffic-from", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"), default=None,
+                    help="instead: turn the counter_collection csv files of two rocprofv3 runs of "
+                         "this script (--pmc FETCH_SIZE, then --pmc WRITE_SIZE) into the fused "
+                         "step's HBM traffic, written to --traffic-out")
+    ap.add_argument("--traffic-out", default=TRAFFIC)
     args = ap.parse_args()
+    if args.traffic_from:
+        traffic_from(args.traffic_from[0], args.traffic_from[1], args.traffic_out,
+                     args.copy_calibration_mb)
+        return
     if args.gpus != 1:
         print(f"bench.py measures one GPU only; --gpus {args.gpus} is not supported "
               f"(sequences shard across GPUs with no exchange, so the per-GPU figure is the one-GPU run)",
