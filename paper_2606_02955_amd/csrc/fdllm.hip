@@ -347,10 +347,7 @@ __device__ __forceinline__ RowResult combine_parts_lanes(const WavePartial& mine
 }
 
 template <int S>
-__device__ __forceinline__ RowResult combine_parts(const WavePartial* part) {
-  WavePartial p[S];
-#pragma unroll
-  for (int q = 0; q < S; ++q) p[q] = part[q];
+__device__ __forceinline__ RowResult combine_parts_regs(const WavePartial (&p)[S]) {
   float M = p[0].m;
 #pragma unroll
   for (int q = 1; q < S; ++q) M = fmaxf(M, p[q].m);
@@ -374,6 +371,14 @@ __device__ __forceinline__ RowResult combine_parts(const WavePartial* part) {
   for (int q = 0; q < S; ++q)
     if (p[q].m == M) first = min(first, p[q].first);
   return finish_row_x(M, K, v[0], first);
+}
+
+template <int S>
+__device__ __forceinline__ RowResult combine_parts(const WavePartial* part) {
+  WavePartial p[S];
+#pragma unroll
+  for (int q = 0; q < S; ++q) p[q] = part[q];
+  return combine_parts_regs<S>(p);
 }
 
 // Row group r of the grid handles the window-relative slot (b, q), q < W =
@@ -716,7 +721,12 @@ __device__ __forceinline__ void select_block_wave(const SelectIO& io, size_t row
 }
 
 // Rows of at most 64 positions: one wavefront per block, four blocks per
-// workgroup.
+// workgroup, lane j for position j of the row.  Every load a lane needs
+// (bounds, mask, conf / eps / token or the wave partials, eta) is addressed
+// by its position alone and issued at once, and the values stay in
+// registers from the pass's outputs to the reveal, so the kernel waits on
+// memory once.  Candidates are ordered by position exactly as in the
+// window-relative form (the slot in the sort key only breaks ties).
 // PS > 0: the candidates' per-position outputs are first formed from their
 // PS wave partials (k_confidence_parts), each by the lane that selects it.
 template <int R, bool Robust, int PS>
@@ -726,19 +736,51 @@ __global__ void __launch_bounds__(256) k_select(SelectIO io, int B, int L, float
   const int b = blockIdx.x * 4 + threadIdx.x / kWave;
   if (b >= B) return;
   const size_t row = (size_t)b * L;
+  const size_t i = row + (size_t)lane;
+  const bool slot = lane < L;
   const int s = io.bstart[b], e_end = io.bend[b];
-  const bool ok = window_ok(s, e_end, L);
-  const int len = ok ? e_end - s : 0;
+  const bool m = slot && io.mask[i] != 0;
+  WavePartial p[PS > 0 ? PS : 1];
+  float c = 0.0f, ef = 1.0f, h = 0.0f;
+  int tok = -1;
   if constexpr (PS > 0) {
-    const size_t i = row + (size_t)(s + lane);
-    if (lane < len && io.mask[i] != 0) store_row(out, i, combine_parts<PS>(parts + i * PS));
+    if (m) {
+#pragma unroll
+      for (int q = 0; q < PS; ++q) p[q] = parts[i * PS + q];
+    }
+  } else {
+    if (m) {
+      c = io.conf[i];
+      if (io.eps) ef = io.eps[i];
+      if (io.x) tok = io.tokens[i];
+    }
   }
-  if (io.commit) {
-    // every entry of row b written once: window slots by their lane, the rest zero
-    for (int q = lane; q < L; q += kWave)
-      if (q < s || q >= s + len) io.commit[row + q] = 0;
+  if constexpr (Robust) h = (m && io.eta.eta) ? io.eta.eta[i] : io.eta.uniform;
+  const bool ok = window_ok(s, e_end, L);
+  const bool inwin = ok && lane >= s && lane < e_end;
+  const bool valid = inwin && m;
+  double e = 1.0;
+  if constexpr (PS > 0) {
+    if (valid) {
+      const RowResult rr = combine_parts_regs<PS>(p);
+      store_row(out, i, rr);
+      c = rr.conf;
+      e = (double)rr.eps;
+      tok = rr.token;
+    }
+  } else if (valid) {
+    e = io.eps ? (double)ef : 1.0 - (double)c;   // 1 - c is exact in double
   }
-  select_block_wave<R, Robust>(io, row, b, s, len, ok, param);
+  if constexpr (Robust) e = valid ? fmin(1.0, e + fmax((double)h, 0.0)) : e;
+  bool take = false;
+  const int nstar = select_wave<R>(valid, e, c, param, take);
+  take = take && valid;
+  if (io.commit && slot) io.commit[i] = take ? 1 : 0;
+  if (take && io.x) {
+    io.x[i] = tok;
+    io.mask[i] = 0;
+  }
+  if (io.n_commit && lane == 0) io.n_commit[b] = ok ? nstar : -1;
 }
 
 // Rows of more than 64 positions: one workgroup per block; blocks of at most
