@@ -225,3 +225,60 @@ class ParityTally:
             with open(path, "a") as fh:
                 fh.write(json.dumps(self.d) + "\n")
         return self.d
+
+
+SHAPES = {
+    "single_block_b1_l32": "B=1, one block of 32, fp32; one step, every row",
+    "generation_b8_g256": ("B=8, 256 positions in blocks of 32, bf16; seven whole generations (one "
+                           "driven by each rule), every step, every sequence"),
+    "sparse_b64_g512": "B=64, span 512, 1..32 masked per block, bf16; one step, every candidate row",
+    "bimodal_b256_g1024": ("B=256, 1024 positions in blocks of 64, bf16; the whole generation (profile "
+                           "f=1 drives it): every step for the 16 flat sequences and 4 others, every "
+                           "sequence at step 0"),
+    "stress_b1024_l32": "B=1024, L=32, bf16, 8.3 GB; one step, every block",
+}
+ORDER = list(SHAPES)
+
+
+def render_report(records) -> str:
+    """Markdown summary of the JSON lines ParityTally appends to FDLLM_PARITY_REPORT."""
+    recs = sorted(records, key=lambda r: ORDER.index(r["workload"]) if r["workload"] in ORDER else 99)
+    out = ["| workload | what is checked | block checks | unflagged mismatches | flagged | flagged and "
+           "matching | row comparisons | worst rel. err conf / eps / lse |",
+           "|---|---|---|---|---|---|---|---|"]
+    tot = dict(block_checks=0, mismatches=0, flagged=0, flagged_matching=0, rows=0)
+    for r in recs:
+        w = r["worst"]
+        out.append(f"| {r['workload']} | {SHAPES.get(r['workload'], '')} | {r['block_checks']} | "
+                   f"{r['mismatches']} | {r['flagged']} | {r['flagged_matching']} | {r['rows']} | "
+                   f"{w['conf']:.1e} / {w['eps']:.1e} / {w['lse']:.1e} |")
+        for k in tot:
+            tot[k] += r[k]
+    out.append(f"| **all** | | **{tot['block_checks']}** | **{tot['mismatches']}** | {tot['flagged']} | "
+               f"{tot['flagged_matching']} | {tot['rows']} | |")
+    out += ["", "Per rule:", "",
+            "| workload | rule | block checks | mismatches | flagged | flagged and matching |",
+            "|---|---|---|---|---|---|"]
+    for r in recs:
+        for rule, st in r["rules"].items():
+            out.append(f"| {r['workload']} | {rule} | {st['block_checks']} | {st['mismatches']} | "
+                       f"{st['flagged']} | {st['flagged_matching']} |")
+    notes = []
+    for r in recs:
+        if "steps_per_generation" in r:
+            notes.append(f"* {r['workload']} steps per whole generation (NFE): " +
+                         ", ".join(f"{k} {v}" for k, v in r["steps_per_generation"].items()) + ".")
+        if "every_step_sequences" in r:
+            notes.append(f"* {r['workload']}: {r.get('steps')} steps; sequences checked at every step: "
+                         f"{r['every_step_sequences']} (flat: {r.get('flat_sequences')}).")
+    if notes:
+        out += [""] + notes
+    return "\n".join(out) + "\n"
+
+
+if __name__ == "__main__":
+    # python tests/parity.py REPORT.jsonl: the markdown tables of a parity run
+    import json
+    import sys
+    with open(sys.argv[1]) as fh:
+        print(render_report([json.loads(line) for line in fh if line.strip()]), end="")
