@@ -14,8 +14,12 @@ Bars (from the method's precision needs):
 """
 from __future__ import annotations
 
+import os
 import sys
 from typing import Iterable, List, Optional, Sequence, Tuple
+
+if __name__ == "__main__":      # run as a script: the repository root is not on the path
+    sys.path.insert(0, os.path.dirname(os.path.dirname(os.path.abspath(__file__))))
 
 import numpy as np
 import torch
