@@ -19,10 +19,13 @@
 //     lane first takes the batch maximum (v_max3), then adds
 //     2^(x*log2e - K) for every element into a double accumulator.  K is an
 //     integer-valued float, K = ceil(m * log2e) for the running maximum m,
-//     so rescaling the accumulator when m grows is an exact ldexp.  The
-//     greedy element enters the sum as exactly the value the final step
-//     recomputes, so s' = sum_{v != t} exp(l_v - M) is recovered by an
-//     exact subtraction and eps keeps its relative accuracy when c -> 1;
+//     so rescaling the accumulator when m grows is an exact ldexp.  No sum
+//     ever holds the greedy element: the batch in which a lane's maximum
+//     appeared is summed apart and, at the row end, again without one
+//     element equal to that maximum, and stretches of a row are merged by
+//     letting all but one holder of the row maximum put their own maximum's
+//     term back; so s' = sum_{v != t} exp(l_v - M) is formed with no
+//     subtraction and eps keeps its relative accuracy when c -> 1;
 //   * the argmax is tracked per batch: each lane keeps, in registers, the
 //     batch in which its maximum first appeared; at the end, lanes holding
 //     the row maximum scan that batch for the lowest index, then a wave
