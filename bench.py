@@ -52,12 +52,39 @@ def log(msg: str):
     print(f"[bench] {msg}", file=sys.stderr, flush=True)
 
 
+def _code_only(text: str) -> str:
+    """C++ source without comments and with whitespace collapsed, so that an
+    edit to comments or layout does not count as a change of the kernel."""
+    import re
+    out, i, n = [], 0, len(text)
+    while i < n:
+        c = text[i]
+        if c in "\"'":                      # string or character literal, kept whole
+            j = i + 1
+            while j < n and text[j] != c:
+                j += 2 if text[j] == "\\" else 1
+            out.append(text[i:j + 1])
+            i = j + 1
+        elif text.startswith("//", i):
+            j = text.find("\n", i)
+            i = n if j < 0 else j
+        elif text.startswith("/*", i):
+            j = text.find("*/", i + 2)
+            i = n if j < 0 else j + 2
+            out.append(" ")
+        else:
+            out.append(c)
+            i += 1
+    return re.sub(r"\s+", " ", "".join(out)).strip()
+
+
 def source_digest() -> str:
-    """Hash of the k_fused sources and the device compiler flags they build with."""
+    """Hash of the k_fused sources (code only: comments and layout do not
+    count) and the device compiler flags they build with."""
     from paper_2606_02955_amd import build as _build
     h = hashlib.sha256()
     for f in SRCS:
-        h.update(open(f, "rb").read())
+        h.update(_code_only(open(f, encoding="utf-8").read()).encode())
     h.update(" ".join(_build.HIPCC_FLAGS).encode())
     return h.hexdigest()[:16]
 

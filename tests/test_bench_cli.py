@@ -46,3 +46,14 @@ def test_traffic_from_counter_runs(tmp_path):
     assert t["fetch_scale"] == 2.0 and t["write_scale"] == 1.0
     assert t["hbm_bytes_per_launch"] == (4000001 * 2.0 + 800) * 1024
     assert t["dispatches"] == {"fetch": {"copy": 1, "fused": 2}, "write": {"copy": 1, "fused": 1}}
+
+
+def test_source_digest_ignores_comments_and_layout():
+    sys.path.insert(0, ROOT)
+    import bench
+    a = 'int f(int x) { // twice\n  return 2 * x; /* done */ }\nconst char* s = "// kept";\n'
+    b = 'int f(int x) {\n\n    return 2 * x;   }\nconst char* s = "// kept";  // the literal stays\n'
+    c = 'int f(int x) { return 3 * x; }\nconst char* s = "// kept";\n'
+    assert bench._code_only(a) == bench._code_only(b)
+    assert bench._code_only(a) != bench._code_only(c)
+    assert '"// kept"' in bench._code_only(a)
