@@ -189,7 +189,13 @@ fdllm_status fdllm_reveal(const uint8_t* commit, const int32_t* tokens, int32_t*
  * One whole decoding step (Alg. 1, loop body after the model call):
  * fdllm_confidence, then the selector `sel` with `param` (f, or tau for the
  * threshold rule), then the reveal, fused.  Large batches run as one kernel
- * (one workgroup per sequence); small batches as two kernels.
+ * (one workgroup per sequence); small batches as two kernels.  When a large
+ * batch exceeds a multiple of the GPU's compute-unit count by at most 64
+ * sequences, those last sequences run with the small-batch kernels on a
+ * stream the library keeps per device, at the same time as the one-kernel
+ * part; the call stays asynchronous (the side stream is forked from and
+ * joined back to `stream` by events).  That needs the workspace, or tokens,
+ * conf and eps all given; without either, they run in the one kernel.
  *   eta, eta_uniform: calibration allowance of FDLLM_SEL_ROBUST (as in
  *   fdllm_select_robust); ignored by the other selectors.
  *   mask [B,L] uint8 (in/out: committed positions are cleared);
@@ -201,7 +207,11 @@ fdllm_status fdllm_reveal(const uint8_t* commit, const int32_t* tokens, int32_t*
  *   and are scratch between calls.  With tokens, conf and eps all given a
  *   smaller workspace (or NULL) is accepted: the results are the same, but a
  *   small batch of blocks of at most 64 positions then streams each row
- *   from one workgroup instead of several.
+ *   from one workgroup instead of several.  (The one exception: a large
+ *   batch's last sequences, above, run in the one kernel when neither the
+ *   workspace nor those three outputs are given; the decisions are the
+ *   oracle's either way, but conf, eps and lse of those sequences are then
+ *   not bitwise fdllm_confidence's.)
  */
 fdllm_status fdllm_decode_step(const void* logits, fdllm_dtype dtype, int B, int L, int V,
                                uint8_t* mask, const int32_t* block_start, const int32_t* block_end,
@@ -393,7 +403,9 @@ fdllm_status fdllm_check_inputs(const void* logits, fdllm_dtype dtype, int B, in
                                 const uint8_t* mask, const int32_t* block_start,
                                 const int32_t* block_end, int32_t* counts, fdllm_stream stream);
 
-/* Workspace bytes fdllm_decode_step needs for these sizes (0 = none). */
+/* Workspace bytes fdllm_decode_step needs for these sizes (0 = none) on the
+ * current device (the large-batch remainder above depends on its
+ * compute-unit count). */
 fdllm_status fdllm_workspace_size(int B, int L, int V, fdllm_dtype dtype, size_t* bytes);
 
 /* Static, human-readable text for a status code. */

@@ -45,6 +45,8 @@
 #include <math.h>
 #include <stdint.h>
 
+#include <mutex>
+
 #include "fdllm.h"
 #include "pass_common.h"
 
@@ -67,6 +69,9 @@
 #endif
 #ifndef FDLLM_FUSED_MIN_B
 #define FDLLM_FUSED_MIN_B 256     // batches from this size run one workgroup per sequence
+#endif
+#ifndef FDLLM_HYBRID_MAX_REM
+#define FDLLM_HYBRID_MAX_REM 64   // sequences beyond a multiple of the CU count run on a side stream
 #endif
 #ifndef FDLLM_WAVES_PER_EU
 #define FDLLM_WAVES_PER_EU 0   // minimum waves per SIMD the fused kernel is compiled for (0: no hint)
@@ -1068,9 +1073,28 @@ struct Plan {
   bool fused;   // one workgroup per sequence, selection in the same kernel
   int split;    // wavefronts per row in the confidence kernel
   int parts;    // decode step with a workspace: split over split / 4 workgroups (0: no)
+  int rem;      // fused: the last rem sequences take the small-batch plan, beside (0: none)
+  int rsplit, rparts;   // that plan's split and parts
 };
 
+// Compute units of the current device (0 when there is none), cached.
+static int device_cus() {
+  static std::mutex mu;
+  static int cus[64];
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 0;
+  std::lock_guard<std::mutex> lock(mu);
+  if (cus[dev] == 0) {
+    int n = 0;
+    if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n < 1)
+      return 0;
+    cus[dev] = n;
+  }
+  return cus[dev];
+}
+
 constexpr int kFusedMinB = FDLLM_FUSED_MIN_B;
+constexpr int kHybridMaxRem = FDLLM_HYBRID_MAX_REM;   // largest remainder run beside the main kernel
 constexpr int kFusedWaves = FDLLM_FUSED_WAVES;   // waves per workgroup in the fused kernel
 constexpr int kTargetWaves = FDLLM_TARGET_WAVES;   // row-streaming waves the split aims for
 
@@ -1079,6 +1103,19 @@ static Plan make_plan(int B, int L, int V, fdllm_dtype dt) {
   const long long win = L < kWaveBlock ? L : kWaveBlock;   // typical block: one wavefront
   p.fused = B >= kFusedMinB;
   p.split = 1;
+  if (p.fused) {
+    // one 8-wave workgroup per sequence fills a CU, so a few sequences beyond
+    // a multiple of the CU count would make a second round that leaves most
+    // CUs idle; they take the small-batch plan instead, on a side stream
+    const int cus = device_cus();
+    const int rem = cus > 0 ? B % cus : 0;
+    if (B > cus && rem <= kHybridMaxRem && rem < kFusedMinB) {
+      const Plan q = make_plan(rem, L, V, dt);
+      p.rem = rem;
+      p.rsplit = q.split;
+      p.rparts = q.parts;
+    }
+  }
   if (!p.fused) {
     // split rows while each part keeps at least 8 16-byte vectors per lane
     const long long row_bytes = (long long)V * (dt == FDLLM_BF16 ? 2 : 4);
@@ -1265,6 +1302,29 @@ static hipError_t launch_fused(fdllm_selector sel, const void* logits, fdllm_dty
                                   n_commit, st);
 }
 
+// A stream of the library's own per device, on which the small-batch
+// remainder of a fused step runs beside the fused kernel (default priority).
+static std::mutex g_side_mu;
+constexpr int kSideDevices = 64;
+static hipStream_t g_side[kSideDevices];
+
+static hipError_t side_stream(hipStream_t* out) {
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= kSideDevices) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lock(g_side_mu);
+  if (!g_side[dev]) {
+    e = hipStreamCreateWithFlags(&g_side[dev], hipStreamNonBlocking);
+    if (e != hipSuccess) {
+      g_side[dev] = nullptr;
+      return e;
+    }
+  }
+  *out = g_side[dev];
+  return hipSuccess;
+}
+
 static bool sizes_ok(int B, int L, int V) {
   if (B < 0 || L < 1 || V < 1) return false;
   const long double total = (long double)B * (long double)L * (long double)V;
@@ -1276,9 +1336,56 @@ static bool sizes_ok(int B, int L, int V) {
 // wave partials of the parts plan
 static size_t out_bytes_for(int B, int L) { return 3 * align256((size_t)B * (size_t)L * 4); }
 static size_t workspace_bytes_for(int B, int L, const Plan& p) {
-  if (p.fused) return 0;
+  if (p.fused) {
+    if (!p.rem) return 0;
+    const size_t n = (size_t)p.rem * (size_t)L;
+    return out_bytes_for(p.rem, L) + (p.rparts ? align256(n * p.rparts * sizeof(WavePartial)) : 0);
+  }
   const size_t n = (size_t)B * (size_t)L;
   return out_bytes_for(B, L) + (p.parts ? align256(n * p.parts * sizeof(WavePartial)) : 0);
+}
+
+// The plan of the small-batch remainder of a fused plan.
+static Plan remainder_plan(const Plan& p) {
+  Plan q{};
+  q.split = p.rsplit;
+  q.parts = p.rparts;
+  return q;
+}
+
+// The small-batch step: the vocabulary pass into the caller's arrays (or
+// the workspace), then one launch that selects and reveals.
+static fdllm_status step_split(const Plan& p, fdllm_selector sel, const void* logits,
+                               fdllm_dtype dtype, int B, int L, int V, uint8_t* mask,
+                               const int32_t* block_start, const int32_t* block_end, int32_t* x,
+                               float param, EtaIn etain, int32_t* tokens, float* conf, float* eps,
+                               float* lse, uint8_t* commit, int32_t* n_commit, void* workspace,
+                               size_t workspace_bytes, hipStream_t st) {
+  const size_t n = (size_t)B * (size_t)L;
+  const bool need_ws = !tokens || !conf || !eps;
+  if (need_ws && (!workspace || workspace_bytes < out_bytes_for(B, L))) return FDLLM_ERR_WORKSPACE;
+  char* ws = (char*)workspace;
+  if (!tokens) tokens = (int32_t*)ws;
+  if (!conf) conf = (float*)(ws + align256(n * 4));
+  if (!eps) eps = (float*)(ws + 2 * align256(n * 4));
+  const RowOut out{tokens, conf, eps, lse};
+  SelectIO io{conf, eps, mask, block_start, block_end, commit, n_commit, tokens, x, etain};
+  hipError_t err;
+  if (p.parts && workspace && workspace_bytes >= out_bytes_for(B, L) +
+                                                     align256(n * p.parts * sizeof(WavePartial))) {
+    // the rows' parts from several workgroups each, combined by the selection
+    // (the same bits as the single-workgroup rows of fdllm_confidence)
+    WavePartial* parts = (WavePartial*)(ws + out_bytes_for(B, L));
+    err = launch_confidence_parts(logits, dtype, B, L, V, p.parts, mask, block_start, block_end, out,
+                                  parts, st);
+    if (err != hipSuccess) return FDLLM_ERR_HIP;
+    err = launch_select(sel, io, B, L, param, st, p.parts, parts, out);
+    return err == hipSuccess ? FDLLM_OK : FDLLM_ERR_HIP;
+  }
+  err = launch_confidence(logits, dtype, B, L, V, p.split, mask, block_start, block_end, out, st);
+  if (err != hipSuccess) return FDLLM_ERR_HIP;
+  err = launch_select(sel, io, B, L, param, st);
+  return err == hipSuccess ? FDLLM_OK : FDLLM_ERR_HIP;
 }
 
 }  // namespace fdllm
@@ -1361,8 +1468,20 @@ fdllm_status fdllm_confidence(const void* logits, fdllm_dtype dtype, int B, int 
   if (!logits || !mask || !block_start || !block_end || !tokens || !conf) return FDLLM_ERR_INVALID_ARG;
   const Plan p = make_plan(B, L, V, dtype);
   RowOut out{tokens, conf, eps, lse};
-  hipError_t err = launch_confidence(logits, dtype, B, L, V, p.split, mask, block_start, block_end,
-                                     out, (hipStream_t)stream);
+  hipStream_t st = (hipStream_t)stream;
+  // the rows of a fused step's small-batch remainder are split as the decode
+  // step splits them, so that both give the same bits
+  const int b0 = B - p.rem;
+  hipError_t err = launch_confidence(logits, dtype, b0, L, V, p.split, mask, block_start, block_end,
+                                     out, st);
+  if (err == hipSuccess && p.rem) {
+    const size_t r0 = (size_t)b0 * (size_t)L;
+    const size_t esize = dtype == FDLLM_BF16 ? 2 : 4;
+    auto off = [](auto* ptr, size_t k) { return ptr ? ptr + k : ptr; };
+    err = launch_confidence((const char*)logits + r0 * (size_t)V * esize, dtype, p.rem, L, V,
+                            p.rsplit, mask + r0, block_start + b0, block_end + b0,
+                            RowOut{off(tokens, r0), off(conf, r0), off(eps, r0), off(lse, r0)}, st);
+  }
   return err == hipSuccess ? FDLLM_OK : FDLLM_ERR_HIP;
 }
 
@@ -1441,37 +1560,46 @@ fdllm_status fdllm_decode_step(const void* logits, fdllm_dtype dtype, int B, int
   if (!logits || !mask || !block_start || !block_end || !x) return FDLLM_ERR_INVALID_ARG;
   const Plan p = make_plan(B, L, V, dtype);
   hipStream_t st = (hipStream_t)stream;
-  RowOut out{tokens, conf, eps, lse};
   const EtaIn etain{eta, eta_uniform};
-  hipError_t err;
-  if (p.fused) {
-    err = launch_fused(sel, logits, dtype, B, L, V, mask, block_start, block_end, x, param, etain,
-                       out, commit, n_commit, st);
-    return err == hipSuccess ? FDLLM_OK : FDLLM_ERR_HIP;
+  if (!p.fused)
+    return step_split(p, sel, logits, dtype, B, L, V, mask, block_start, block_end, x, param, etain,
+                      tokens, conf, eps, lse, commit, n_commit, workspace, workspace_bytes, st);
+  RowOut out{tokens, conf, eps, lse};
+  const int b0 = B - p.rem;
+  const Plan q = remainder_plan(p);
+  const bool outs_given = tokens && conf && eps;
+  hipStream_t side = nullptr;
+  if (p.rem && (outs_given || (workspace && workspace_bytes >= workspace_bytes_for(B, L, p))) &&
+      side_stream(&side) == hipSuccess) {
+    // sequences [b0, B) on the side stream, forked from and joined back to
+    // the caller's stream by events, at the same time as the fused kernel
+    const size_t r0 = (size_t)b0 * (size_t)L;
+    const size_t esize = dtype == FDLLM_BF16 ? 2 : 4;
+    auto off = [](auto* ptr, size_t k) { return ptr ? ptr + k : ptr; };
+    hipEvent_t fork = nullptr, join = nullptr;
+    fdllm_status res = FDLLM_ERR_HIP;
+    if (hipEventCreateWithFlags(&fork, hipEventDisableTiming) == hipSuccess &&
+        hipEventCreateWithFlags(&join, hipEventDisableTiming) == hipSuccess &&
+        hipEventRecord(fork, st) == hipSuccess && hipStreamWaitEvent(side, fork, 0) == hipSuccess) {
+      res = step_split(q, sel, (const char*)logits + r0 * (size_t)V * esize, dtype, p.rem, L, V,
+                       mask + r0, block_start + b0, block_end + b0, x + r0, param,
+                       EtaIn{off(eta, r0), eta_uniform}, off(tokens, r0), off(conf, r0),
+                       off(eps, r0), off(lse, r0), off(commit, r0), off(n_commit, (size_t)b0),
+                       workspace, workspace_bytes, side);
+      if (res == FDLLM_OK && hipEventRecord(join, side) != hipSuccess) res = FDLLM_ERR_HIP;
+      if (res == FDLLM_OK &&
+          launch_fused(sel, logits, dtype, b0, L, V, mask, block_start, block_end, x, param, etain,
+                       out, commit, n_commit, st) != hipSuccess)
+        res = FDLLM_ERR_HIP;
+      if (res == FDLLM_OK && hipStreamWaitEvent(st, join, 0) != hipSuccess) res = FDLLM_ERR_HIP;
+    }
+    // a recorded event's resources are released once it completes
+    if (fork) (void)hipEventDestroy(fork);
+    if (join) (void)hipEventDestroy(join);
+    return res;
   }
-  // two kernels: confidence into the caller's arrays or the workspace, then select+reveal
-  const size_t n = (size_t)B * (size_t)L;
-  const bool need_ws = !tokens || !conf || !eps;
-  if (need_ws && (!workspace || workspace_bytes < out_bytes_for(B, L))) return FDLLM_ERR_WORKSPACE;
-  char* ws = (char*)workspace;
-  if (!tokens) tokens = (int32_t*)ws;
-  if (!conf) conf = (float*)(ws + align256(n * 4));
-  if (!eps) eps = (float*)(ws + 2 * align256(n * 4));
-  out = RowOut{tokens, conf, eps, lse};
-  SelectIO io{conf, eps, mask, block_start, block_end, commit, n_commit, tokens, x, etain};
-  if (p.parts && workspace && workspace_bytes >= workspace_bytes_for(B, L, p)) {
-    // the rows' parts from several workgroups each, combined by the selection
-    // (the same bits as the single-workgroup rows of fdllm_confidence)
-    WavePartial* parts = (WavePartial*)(ws + out_bytes_for(B, L));
-    err = launch_confidence_parts(logits, dtype, B, L, V, p.parts, mask, block_start, block_end, out,
-                                  parts, st);
-    if (err != hipSuccess) return FDLLM_ERR_HIP;
-    err = launch_select(sel, io, B, L, param, st, p.parts, parts, out);
-    return err == hipSuccess ? FDLLM_OK : FDLLM_ERR_HIP;
-  }
-  err = launch_confidence(logits, dtype, B, L, V, p.split, mask, block_start, block_end, out, st);
-  if (err != hipSuccess) return FDLLM_ERR_HIP;
-  err = launch_select(sel, io, B, L, param, st);
+  const hipError_t err = launch_fused(sel, logits, dtype, B, L, V, mask, block_start, block_end, x,
+                                      param, etain, out, commit, n_commit, st);
   return err == hipSuccess ? FDLLM_OK : FDLLM_ERR_HIP;
 }
 

@@ -11,7 +11,7 @@ import torch
 import oracle
 import workloads
 from parity import (say, row_source, candidates, compare_rows, gpu_confidence,
-                    oracle_confidence_subset, check_defaults, compare_selection)
+                    oracle_confidence_subset, check_defaults, compare_selection, sub_mask)
 
 pytestmark = pytest.mark.gpu
 
@@ -368,6 +368,44 @@ def test_decode_step_row_parts_match_single_workgroup(gpu, B, L, V, dt, window):
     assert torch.equal(m1, m2) and torch.equal(x1, x2)
     for k in o1:
         assert torch.equal(o1[k].view(torch.uint8), o2[k].view(torch.uint8)), k
+
+
+@pytest.mark.parametrize("B,L,V,dt,window", [(260, 32, 126464, torch.bfloat16, 32),
+                                              (300, 12, 20000, torch.float32, 12),
+                                              (257, 70, 3000, torch.bfloat16, 70)])
+def test_fused_step_remainder_bits(gpu, B, L, V, dt, window):
+    """Sequences beyond a multiple of the CU count take the small-batch plan
+    beside the fused kernel: the decode step gives fdllm_confidence's bits for
+    every row, the same with and without a workspace, and the oracle's
+    results (checked on the remainder and a few fused sequences)."""
+    inp = _case(B, L, V, dt, window, seed=B + L)
+    say(f"[fused step remainder] {inp.name}")
+    ref = gpu_confidence(gpu, inp)
+    outs = []
+    for ws in ("default", None):
+        mask, x = inp.mask.clone(), inp.x.clone()
+        o = {"tokens": torch.full((B, L), -7, dtype=torch.int32, device="cuda"),
+             "conf": torch.full((B, L), -7.0, device="cuda"),
+             "eps": torch.full((B, L), -7.0, device="cuda"),
+             "lse": torch.full((B, L), -7.0, device="cuda"),
+             "commit": torch.full((B, L), 9, dtype=torch.uint8, device="cuda"),
+             "n_commit": torch.full((B,), -9, dtype=torch.int32, device="cuda")}
+        kw = {} if ws == "default" else {"workspace": torch.empty(1, dtype=torch.uint8, device="cuda")}
+        gpu.fdllm_decode_step(inp.logits, mask, inp.start, inp.end, x, "profile", 1.0, **kw, **o)
+        torch.cuda.synchronize()
+        outs.append((mask, x, o))
+    (m1, x1, o1), (m2, x2, o2) = outs
+    assert torch.equal(m1, m2) and torch.equal(x1, x2)
+    for k in o1:
+        assert torch.equal(o1[k].view(torch.uint8), o2[k].view(torch.uint8)), k
+    for k, t in zip(("tokens", "conf", "eps", "lse"), ref):
+        assert torch.equal(o1[k].view(torch.uint8), t.view(torch.uint8)), k
+    bs = [0, 1, 100] + list(range(B - 8, B))
+    m0, x0 = sub_mask(inp.mask.cpu().numpy(), bs), inp.x.cpu().numpy()
+    r = oracle.decode_step(row_source(inp.logits), B, L, m0, inp.start.cpu().numpy(),
+                           inp.end.cpu().numpy(), x0, "profile", 1.0)
+    compare_selection(o1["commit"].cpu().numpy(), o1["n_commit"].cpu().numpy(), r.commit,
+                      r.n_commit, r.flagged, bs)
 
 
 def _random_shapes(n, seed=2606):
