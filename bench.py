@@ -505,8 +505,9 @@ def plan_sweep(reps: int, md_path):
     """Cold decode-step times over the batch size B and the masked rows per
     block m (L = 32, V = 126464 bf16, profile f = 1): the plan the library
     picks at each B (one workgroup per sequence from 256 sequences, rows split
-    over waves plus a selection launch below).  One JSON line; optionally a
-    markdown table."""
+    over waves plus a selection launch below; up to 64 sequences beyond a
+    multiple of the CU count take the split plan on a side stream beside the
+    fused kernel).  One JSON line; optionally a markdown table."""
     import torch
     import paper_2606_02955_amd as fd
     fd.load()
@@ -519,6 +520,16 @@ def plan_sweep(reps: int, md_path):
     for b0 in range(0, big.shape[0], 64):
         big[b0:b0 + 64].normal_(generator=g)
     scratch = torch.empty(512 << 20, dtype=torch.uint8, device=dev)
+    cus = torch.cuda.get_device_properties(dev).multi_processor_count
+
+    def plan_name(B):
+        if B < 256:
+            return "rows split over waves + selection"
+        rem = B % cus
+        if 0 < rem <= 64:
+            return f"one workgroup per sequence for {B - rem}, split rows for {rem} on a side stream"
+        return "one workgroup per sequence"
+
     res = []
     for B in Bs:
         logits = big[:B]
@@ -546,7 +557,7 @@ def plan_sweep(reps: int, md_path):
             t = sorted(ts)[len(ts) // 2]
             nbytes = B * m * V * 2
             res.append({"B": B, "m": m, "us": t * 1e6, "GBps": nbytes / t / 1e9,
-                        "plan": "one workgroup per sequence" if B >= 256 else "rows split over waves + selection"})
+                        "plan": plan_name(B)})
             log(f"plan sweep B={B} m={m}: {t * 1e6:.1f} us, {nbytes / t / 1e9:.0f} GB/s")
     print(json.dumps({"metric": "decode-step time over batch size and masked rows per block (cold)",
                       "L": L, "V": V, "dtype": "bf16", "reps": reps, "rows": res}), flush=True)
@@ -555,7 +566,9 @@ def plan_sweep(reps: int, md_path):
                f"    python bench.py --plan-sweep --plan-sweep-md <file>", "",
                "Cold decode steps (512 MB overwritten before each), L = 32, V = 126464 bf16, profile f = 1, "
                f"median of {reps}; m of the 32 positions of every block masked.  B >= 256 runs one workgroup "
-               "per sequence, smaller batches the split rows plus a selection launch.  Cells: µs (logits GB/s).", "",
+               "per sequence, smaller batches the split rows plus a selection launch; beyond a multiple of "
+               f"the {cus} CUs, up to 64 sequences run the split plan on a side stream beside the fused "
+               "kernel (B = 320 here).  Cells: µs (logits GB/s).", "",
                "| B | " + " | ".join(f"m = {m}" for m in ms) + " |", "|---|" + "---|" * len(ms)]
         for B in Bs:
             cells = [r for r in res if r["B"] == B]
