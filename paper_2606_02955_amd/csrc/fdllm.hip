@@ -179,6 +179,18 @@ __device__ __forceinline__ WavePartial row_pass(const typename Vec::Raw* __restr
 #pragma unroll
   for (int u = 0; u < U; ++u) keep[u] = Vec::pad();
 
+  // sum of a batch's terms: kAcc accumulators, each started from its first
+  // term (as 0 + t would give, without the add), then a fixed pairing
+  static_assert(U * E >= kAcc, "a batch fills every accumulator");
+  auto batch_sum = [&](const float (&x)[U][E]) {
+    double t[kAcc];
+#pragma unroll
+    for (int a = 0; a < kAcc; ++a) t[a] = (double)term(x[a / E][a % E], K);
+#pragma unroll
+    for (int i = kAcc; i < U * E; ++i) t[i % kAcc] += (double)term(x[i / E][i % E], K);
+    return (t[0] + t[1]) + (t[2] + t[3]);
+  };
+
   auto consume = [&](const Raw (&r)[U], int batch) {
     float x[U][E];
 #pragma unroll
@@ -200,14 +212,7 @@ __device__ __forceinline__ WavePartial row_pass(const typename Vec::Raw* __restr
     pend = rescale(pend, K, Kn);
     m = mn;
     K = Kn;
-    double t[kAcc];
-#pragma unroll
-    for (int a = 0; a < kAcc; ++a) t[a] = 0.0;
-#pragma unroll
-    for (int u = 0; u < U; ++u)
-#pragma unroll
-      for (int e = 0; e < E; ++e) t[(u * E + e) % kAcc] += (double)term(x[u][e], K);
-    const double bs = (t[0] + t[1]) + (t[2] + t[3]);
+    const double bs = batch_sum(x);
     // a new kept batch sends the previous one's terms to acc
     acc += grows ? pend : bs;
     pend = grows ? bs : pend;

@@ -99,17 +99,25 @@ __device__ __forceinline__ int wave_min(int v) {
 // ---------------------------------------------------------------------------
 //
 // exp_ref(m) is the smallest integer K >= m * log2e (log2e taken as the float
-// kLog2e).  The product of two floats is exact in double and ceil() of it is
-// exact, so for |m| <= FDLLM_MAX_ABS_LOGIT (|K| < 2^24, a float) the maximum's
-// own argument m * log2e - K lies in (-1, 0] at every magnitude and its term
-// in (1/2, 1].  (A float product rounds to a grid coarser than 1 once
-// |m log2e| >= 2^24, and its ceiling can then sit far from the exact one.)
-// Outside that range K is rounded up to the next float, so the argument stays
-// <= 0 and no term overflows.
+// kLog2e), so for |m| <= FDLLM_MAX_ABS_LOGIT (|K| < 2^24, a float) the
+// maximum's own argument m * log2e - K lies in (-1, 0] at every magnitude and
+// its term in (1/2, 1].  It is formed in float arithmetic without rounding
+// error: p = fl(m log2e) and e = fma(m, log2e, -p) = m log2e - p exactly (the
+// error of a rounded product is a float).  While |p| < 2^24 the integers are
+// on p's grid and |e| is at most half its spacing, so the exact product and p
+// have the same ceiling unless p is itself an integer, and then the ceiling
+// is p + 1 exactly when e > 0.  (The ceiling of p alone can leave the
+// maximum's argument above 0.)  Beyond 2^24, outside the documented range, K
+// is the next float above ceil(p), an integer >= the exact product, so the
+// argument stays <= 0 and no term overflows.
 __device__ __forceinline__ float exp_ref(float m) {
-  const double k = ceil((double)m * (double)kLog2e);
-  const float kf = (float)k;
-  return (double)kf < k ? __int_as_float(__float_as_int(kf) + (kf > 0.0f ? 1 : -1)) : kf;
+  const float p = m * kLog2e;
+  const float e = __builtin_fmaf(m, kLog2e, -p);
+  const float c = __builtin_ceilf(p);
+  const float in_range = (c == p && e > 0.0f) ? c + 1.0f : c;
+  const float next = __int_as_float(__float_as_int(c) + (c > 0.0f ? 1 : -1));
+  const float beyond = __builtin_isinf(c) ? c : next;
+  return __builtin_fabsf(c) < 16777216.0f ? in_range : beyond;
 }
 __device__ __forceinline__ float term(float x, float K) {
   return __builtin_amdgcn_exp2f(__builtin_fmaf(x, kLog2e, -K));

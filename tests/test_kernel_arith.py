@@ -28,14 +28,31 @@ LOG2E_F = np.float32(1.44269504088896340736)
 MAX_ABS_LOGIT = 1.0e7
 
 
-def exp_ref(m: np.float32) -> np.float32:
-    """Smallest integer >= m * log2e, from the exact double product, rounded
-    up to a float when it is not one."""
+def exp_ref_exact(m: np.float32) -> np.float32:
+    """The definition: the smallest integer >= m * log2e, from the exact
+    double product (two floats' product fits a double's 53 bits), rounded up
+    to a float when it is not one."""
     k = math.ceil(float(m) * float(LOG2E_F))
     kf = np.float32(k)
     if float(kf) < k:
         kf = np.nextafter(kf, np.float32(np.inf))
     return kf
+
+
+def exp_ref(m: np.float32) -> np.float32:
+    """The kernel's float formulation: p = fl(m log2e), the sign of the exact
+    remainder m log2e - p (what fma(m, log2e, -p) returns), c = ceil(p); K =
+    c + 1 when p is an integer below the exact product, else c; beyond 2^24
+    the next float above c."""
+    m = np.float32(m)
+    p = np.float32(m * LOG2E_F)
+    e = float(m) * float(LOG2E_F) - float(p)     # exact in double
+    c = np.float32(np.ceil(p))
+    if abs(c) < np.float32(16777216.0):
+        return np.float32(c + np.float32(1.0)) if (c == p and e > 0.0) else c
+    if np.isinf(c):
+        return c
+    return np.nextafter(c, np.float32(np.inf))
 
 
 def exp_ref_float_product(m: np.float32) -> np.float32:
@@ -152,6 +169,28 @@ def test_maximum_argument_in_range(M):
         m = np.float32(np.clip(m, -MAX_ABS_LOGIT, MAX_ABS_LOGIT))
         a = arg(m, exp_ref(m))
         assert -1.0 < a <= 0.0, (m, a)
+
+
+def test_float_formulation_is_the_exact_ceiling_in_range():
+    # the kernel forms K in float arithmetic; within |m| <= 1e7 it must equal
+    # the ceiling of the exact product everywhere: random magnitudes, values
+    # whose rounded product is an integer (the remainder's sign decides), and
+    # the neighbours of those
+    rng = np.random.default_rng(5)
+    ms = [np.float32(v) for v in rng.uniform(-MAX_ABS_LOGIT, MAX_ABS_LOGIT, 20000)]
+    ms += [np.float32(v) for v in rng.normal(0.0, 30.0, 20000)]
+    hits = 0
+    for k in rng.integers(-(1 << 23), 1 << 23, 20000):
+        m0 = np.float32(float(k) / float(LOG2E_F))
+        for m in (np.nextafter(m0, np.float32(-np.inf)), m0, np.nextafter(m0, np.float32(np.inf))):
+            if abs(m) <= MAX_ABS_LOGIT:
+                ms.append(m)
+                hits += int(np.float32(m * LOG2E_F) == np.ceil(np.float32(m * LOG2E_F)))
+    ms += [np.float32(0.0), np.float32(-0.0), np.float32(1e-45), np.float32(-1e-45),
+           np.float32(MAX_ABS_LOGIT), np.float32(-MAX_ABS_LOGIT)]
+    assert hits > 10000           # many rounded products are integers
+    for m in ms:
+        assert exp_ref(m) == exp_ref_exact(m), m
 
 
 def test_float_product_reference_was_not_exact():
