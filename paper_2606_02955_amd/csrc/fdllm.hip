@@ -154,7 +154,8 @@ constexpr int kAcc = 4;   // independent double accumulators per lane
 // The wave handles wave-loads k = w, w+S, w+2S, ... of the row (a wave-load
 // is 64 consecutive vectors); lane l reads vector k*64 + l.
 template <class Vec, int U, int S>
-__device__ __forceinline__ WavePartial row_pass(const typename Vec::Raw* __restrict__ row, int nvec, int w) {
+__device__ __forceinline__ WavePartial row_pass(const typename Vec::Raw* __restrict__ row, int nvec, int w,
+                                                typename Vec::Raw* __restrict__ kept) {
   using Raw = typename Vec::Raw;
   constexpr int E = Vec::kElems;
   const int lane = lane_id();
@@ -171,13 +172,13 @@ __device__ __forceinline__ WavePartial row_pass(const typename Vec::Raw* __restr
   // batch's terms, dropped at the end, where the kept batch is summed again
   // without one element equal to m (so no sum ever holds the lane maximum)
   double acc = 0.0, pend = 0.0;
-  // the batch in which this lane's maximum first appeared, and its vectors:
-  // the lowest index of the row maximum is found in registers at the end
-  // (a re-read from memory would cost a dependent HBM latency per row)
+  // the batch in which this lane's maximum first appeared, and its vectors,
+  // kept in this wave's LDS area `kept` (2 U kWave vectors): every batch is
+  // written there, a lane whose maximum grows into slot 0 (u kWave + lane),
+  // the others into slot 1, so no per-lane select is needed; the lowest index
+  // of the row maximum is found there at the end (a re-read from memory
+  // would cost a dependent HBM latency per row)
   int rec = -1;
-  Raw keep[U];
-#pragma unroll
-  for (int u = 0; u < U; ++u) keep[u] = Vec::pad();
 
   // sum of a batch's terms: kAcc accumulators, each started from its first
   // term (as 0 + t would give, without the add), then a fixed pairing
@@ -202,8 +203,9 @@ __device__ __forceinline__ WavePartial row_pass(const typename Vec::Raw* __restr
       for (int e = 0; e < E; ++e) bm = fmaxf(bm, x[u][e]);
     const bool grows = bm > m;
     rec = grows ? batch : rec;
+    Raw* const dst = kept + (grows ? 0 : U * kWave) + lane;
 #pragma unroll
-    for (int u = 0; u < U; ++u) keep[u] = grows ? r[u] : keep[u];
+    for (int u = 0; u < U; ++u) dst[u * kWave] = r[u];
     const float mn = fmaxf(m, bm);
     // a lane that has only seen padding keeps a finite reference, so that
     // padding terms are exp2(-inf) = 0 rather than exp2(-inf + inf)
@@ -264,6 +266,9 @@ __device__ __forceinline__ WavePartial row_pass(const typename Vec::Raw* __restr
 
   // the kept batch again, without one element equal to the lane maximum
   // (padding is -inf: its terms are 0)
+  Raw keep[U];
+#pragma unroll
+  for (int u = 0; u < U; ++u) keep[u] = rec >= 0 ? kept[u * kWave + lane] : Vec::pad();
   double s = acc;
   if (rec >= 0) {
     bool left_out = false;
@@ -406,6 +411,7 @@ k_confidence(const typename Vec::Raw* __restrict__ logits, int B, int L, int nve
              const int32_t* __restrict__ bend, RowOut out) {
   using Shape = SplitShape<S>;
   __shared__ WavePartial part[Shape::kWaves];
+  __shared__ typename Vec::Raw s_kept[2 * U * Shape::kThreads];
   const int wave = threadIdx.x / kWave;
   const int lane = threadIdx.x % kWave;
   const int rloc = wave / S;
@@ -436,7 +442,7 @@ k_confidence(const typename Vec::Raw* __restrict__ logits, int B, int L, int nve
     const size_t slot = row0 + (size_t)(s + rel);
     const bool cand = inwin && mask[slot] != 0;
     WavePartial wp{};
-    if (cand) wp = row_pass<Vec, U, S>(logits + (long long)slot * nvec, nvec, w);
+    if (cand) wp = row_pass<Vec, U, S>(logits + (long long)slot * nvec, nvec, w, s_kept + wave * 2 * U * kWave);
     if constexpr (S > 1) {
       if (lane == 0) part[wave] = wp;
       __syncthreads();
@@ -468,6 +474,7 @@ k_confidence_parts(const typename Vec::Raw* __restrict__ logits, int B, int L, i
                    const uint8_t* __restrict__ mask, const int32_t* __restrict__ bstart,
                    const int32_t* __restrict__ bend, RowOut out, WavePartial* __restrict__ parts) {
   constexpr int P = S / 4;                                  // workgroups per slot
+  __shared__ typename Vec::Raw s_kept[2 * U * 256];
   const int wave = threadIdx.x / kWave;
   const int lane = threadIdx.x % kWave;
   const long long slot = blockIdx.x / P;
@@ -479,7 +486,7 @@ k_confidence_parts(const typename Vec::Raw* __restrict__ logits, int B, int L, i
     if (w == 0 && lane == 0) store_default(out, (size_t)slot);
     return;
   }
-  const WavePartial wp = row_pass<Vec, U, S>(logits + slot * (long long)nvec, nvec, w);
+  const WavePartial wp = row_pass<Vec, U, S>(logits + slot * (long long)nvec, nvec, w, s_kept + wave * 2 * U * kWave);
   if (lane == 0) parts[slot * S + w] = wp;
 }
 
@@ -861,6 +868,7 @@ k_fused(const typename Vec::Raw* __restrict__ logits, int B, int L, int nvec,
         const int32_t* __restrict__ bend, int32_t* __restrict__ x, float param, EtaIn eta,
         RowOut out, uint8_t* __restrict__ commit, int32_t* __restrict__ n_commit) {
   __shared__ int s_cand[kWaveBlock];      // candidate slots, compacted
+  __shared__ typename Vec::Raw s_kept[2 * U * W * kWave];
   __shared__ int s_tok[kWaveBlock];
   __shared__ float s_conf[kWaveBlock];
   __shared__ float s_eps[kWaveBlock];
@@ -892,7 +900,7 @@ k_fused(const typename Vec::Raw* __restrict__ logits, int B, int L, int nvec,
   for (int c = wave; c < m; c += W) {
     const int slot = s_cand[c];
     const size_t r = row0 + s + slot;
-    const WavePartial wp = row_pass<Vec, U, 1>(logits + r * (size_t)nvec, nvec, 0);
+    const WavePartial wp = row_pass<Vec, U, 1>(logits + r * (size_t)nvec, nvec, 0, s_kept + wave * 2 * U * kWave);
     const RowResult rr = finish_row_x(wp.m, wp.K, wp.S, wp.first);
     if (lane == 0) {
       store_row(out, r, rr);
@@ -932,6 +940,7 @@ k_fused_wide(const typename Vec::Raw* __restrict__ logits, int B, int L, int nve
   constexpr int NT = W * kWave;
   __shared__ WideLds sh;
   __shared__ int s_cand[kMaxBlock];       // candidate slots, compacted
+  __shared__ typename Vec::Raw s_kept[2 * U * W * kWave];
   const int b = blockIdx.x;
   const int tid = threadIdx.x;
   const int wave = tid / kWave;
@@ -963,7 +972,7 @@ k_fused_wide(const typename Vec::Raw* __restrict__ logits, int B, int L, int nve
   for (int c = wave; c < m; c += W) {
     const int slot = s_cand[c];
     const size_t r = row0 + s + slot;
-    const WavePartial wp = row_pass<Vec, U, 1>(logits + r * (size_t)nvec, nvec, 0);
+    const WavePartial wp = row_pass<Vec, U, 1>(logits + r * (size_t)nvec, nvec, 0, s_kept + wave * 2 * U * kWave);
     const RowResult rr = finish_row_x(wp.m, wp.K, wp.S, wp.first);
     if (lane == 0) {
       store_row(out, r, rr);
