@@ -70,6 +70,9 @@
 #ifndef FDLLM_FUSED_MIN_B
 #define FDLLM_FUSED_MIN_B 256     // batches from this size run one workgroup per sequence
 #endif
+#ifndef FDLLM_ROW_GROUPS
+#define FDLLM_ROW_GROUPS 64       // small batches: window-relative row groups per sequence (at most)
+#endif
 #ifndef FDLLM_HYBRID_MAX_REM
 #define FDLLM_HYBRID_MAX_REM 64   // sequences beyond a multiple of the CU count run on a side stream
 #endif
@@ -78,6 +81,9 @@
 #endif
 
 namespace fdllm {
+constexpr int kRowGroups = FDLLM_ROW_GROUPS;   // row groups per sequence of the split pass (at most)
+static_assert(kRowGroups >= 1 && kRowGroups <= 64, "row groups");
+
 // ---------------------------------------------------------------------------
 // vector formats: one lane loads 16 bytes (or one element on the scalar path)
 // ---------------------------------------------------------------------------
@@ -416,7 +422,7 @@ k_confidence(const typename Vec::Raw* __restrict__ logits, int B, int L, int nve
   const int lane = threadIdx.x % kWave;
   const int rloc = wave / S;
   const int w = wave % S;
-  const int W = L < kWaveBlock ? L : kWaveBlock;
+  const int W = L < kRowGroups ? L : kRowGroups;
   const long long vs = (long long)blockIdx.x * Shape::kRows + rloc;
   const bool live = vs < (long long)B * W;
   int b = 0, q = 0, s = 0, len = 0;
@@ -1114,7 +1120,7 @@ constexpr int kTargetWaves = FDLLM_TARGET_WAVES;   // row-streaming waves the sp
 
 static Plan make_plan(int B, int L, int V, fdllm_dtype dt) {
   Plan p{};
-  const long long win = L < kWaveBlock ? L : kWaveBlock;   // typical block: one wavefront
+  const long long win = L < kRowGroups ? L : kRowGroups;
   p.fused = B >= kFusedMinB;
   p.split = 1;
   if (p.fused) {
@@ -1152,7 +1158,7 @@ template <class Vec>
 static hipError_t launch_confidence_t(const void* logits, int B, int L, int nvec, int split,
                                       const uint8_t* mask, const int32_t* bs, const int32_t* be,
                                       RowOut out, hipStream_t st) {
-  const long long nvslots = (long long)B * (L < kWaveBlock ? L : kWaveBlock);   // window-relative
+  const long long nvslots = (long long)B * (L < kRowGroups ? L : kRowGroups);   // window-relative
   const auto* lg = (const typename Vec::Raw*)logits;
 #define FDLLM_CONF_CASE(SPLIT)                                                                  \
   case SPLIT: {                                                                                 \
