@@ -382,6 +382,11 @@ fdllm_status fdllm_generation_create(const fdllm_generation_desc* desc, fdllm_ge
  */
 fdllm_status fdllm_generation_run(fdllm_generation gen, fdllm_stream stream, int32_t* steps);
 
+/*
+ * Releases the object's graph, capture stream, events and pinned memory (all
+ * of them, also when one release fails; FDLLM_ERR_HIP then).  NULL is a
+ * no-op.  The caller's buffers are not touched.
+ */
 fdllm_status fdllm_generation_destroy(fdllm_generation gen);
 
 /*

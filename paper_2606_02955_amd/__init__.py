@@ -410,8 +410,8 @@ class Generation:
 
     def close(self):
         if getattr(self, "handle", None) and self.handle.value:
-            self.lib.fdllm_generation_destroy(self.handle)
-            self.handle = ctypes.c_void_p(0)
+            h, self.handle = self.handle, ctypes.c_void_p(0)
+            _check(self.lib.fdllm_generation_destroy(h), "fdllm_generation_destroy")
 
     def __del__(self):
         try:

@@ -345,14 +345,19 @@ fdllm_status fdllm_generation_run(fdllm_generation g, fdllm_stream stream, int32
 
 fdllm_status fdllm_generation_destroy(fdllm_generation g) {
   if (!g) return FDLLM_OK;
-  if (g->exec) hipGraphExecDestroy(g->exec);
-  if (g->graph) hipGraphDestroy(g->graph);
-  if (g->cap) hipStreamDestroy(g->cap);
-  if (g->ev[0]) hipEventDestroy(g->ev[0]);
-  if (g->ev[1]) hipEventDestroy(g->ev[1]);
-  if (g->host_active) hipHostFree(g->host_active);
+  // every resource is released; the first failure is reported
+  hipError_t first = hipSuccess;
+  auto note = [&first](hipError_t e) {
+    if (first == hipSuccess) first = e;
+  };
+  if (g->exec) note(hipGraphExecDestroy(g->exec));
+  if (g->graph) note(hipGraphDestroy(g->graph));
+  if (g->cap) note(hipStreamDestroy(g->cap));
+  if (g->ev[0]) note(hipEventDestroy(g->ev[0]));
+  if (g->ev[1]) note(hipEventDestroy(g->ev[1]));
+  if (g->host_active) note(hipHostFree(g->host_active));
   free(g);
-  return FDLLM_OK;
+  return first == hipSuccess ? FDLLM_OK : FDLLM_ERR_HIP;
 }
 
 }  // extern "C"
