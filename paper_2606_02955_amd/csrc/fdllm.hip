@@ -26,8 +26,8 @@
 //     letting all but one holder of the row maximum put their own maximum's
 //     term back; so s' = sum_{v != t} exp(l_v - M) is formed with no
 //     subtraction and eps keeps its relative accuracy when c -> 1;
-//   * the argmax is tracked per batch: each lane keeps, in registers, the
-//     batch in which its maximum first appeared; at the end, lanes holding
+//   * the argmax is tracked per batch: each lane keeps, in LDS, the batch
+//     in which its maximum first appeared; at the end, lanes holding
 //     the row maximum scan that batch for the lowest index, then a wave
 //     minimum gives the lowest index of the whole row;
 //   * wavefront reductions use DPP row operations, ds_swizzle and
