@@ -486,8 +486,10 @@ k_confidence_parts(const typename Vec::Raw* __restrict__ logits, int B, int L, i
   const long long slot = blockIdx.x / P;
   const int w = (int)(blockIdx.x % P) * 4 + wave;           // part of the row
   const int b = (int)(slot / L), i = (int)(slot % L);
+  // the mask byte and the bounds are read together (one round trip)
+  const bool masked = mask[slot] != 0;
   const int s = bstart[b], e = bend[b];
-  const bool cand = window_ok(s, e, L) && i >= s && i < e && mask[slot] != 0;
+  const bool cand = masked & window_ok(s, e, L) & (i >= s) & (i < e);
   if (!cand) {
     if (w == 0 && lane == 0) store_default(out, (size_t)slot);
     return;
@@ -727,20 +729,30 @@ __device__ __forceinline__ void select_block_wave(const SelectIO& io, size_t row
                                                   int len, bool ok, float param) {
   const int lane = lane_id();
   const bool inwin = lane < len;
-  const size_t i = row + (size_t)(s + lane);
-  const bool valid = inwin && io.mask[i] != 0;
-  float c = 0.0f;
+  // every lane issues all of its loads at once (lanes past the window read
+  // the row's first slot, in bounds, and discard it; absent arrays are stood
+  // in for by conf); the fences keep the loads ahead of the arithmetic
+  const size_t i = row + (inwin ? (size_t)(s + lane) : 0);
+  const uint8_t mb = io.mask[i];
+  const float cv = io.conf[i];
+  const float ev = (io.eps ? io.eps : io.conf)[i];
+  const int32_t tv = (io.x ? io.tokens : reinterpret_cast<const int32_t*>(io.conf))[i];
+  float hv = 0.0f;
+  if constexpr (Robust) hv = (io.eta.eta ? io.eta.eta : io.conf)[i];
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_sched_barrier(0);
+  const bool valid = inwin && mb != 0;
+  const float c = valid ? cv : 0.0f;
   double e = 1.0;
   if (valid) {
-    c = io.conf[i];
-    e = cand_eps(io.eps, c, i);
-    if constexpr (Robust) e = robust_eps(e, io.eta, i);
+    e = io.eps ? (double)ev : 1.0 - (double)c;   // 1 - c is exact in double
+    if constexpr (Robust) e = fmin(1.0, e + fmax((double)(io.eta.eta ? hv : io.eta.uniform), 0.0));
   }
   bool take = false;
   const int nstar = select_wave<R>(valid, e, c, param, take);
   if (io.commit && inwin) io.commit[i] = take ? 1 : 0;
   if (take && io.x) {
-    io.x[i] = io.tokens[i];
+    io.x[i] = tv;
     io.mask[i] = 0;
   }
   if (io.n_commit && lane == 0) io.n_commit[b] = ok ? nstar : -1;
@@ -764,38 +776,57 @@ __global__ void __launch_bounds__(256) k_select(SelectIO io, int B, int L, float
   const size_t row = (size_t)b * L;
   const size_t i = row + (size_t)lane;
   const bool slot = lane < L;
+  // every load of the kernel is issued before any of them returns: each lane
+  // reads its slot's mask byte, outputs (or wave partials) and eta whether or
+  // not the slot turns out to be a candidate, lanes past the row reading the
+  // row's first slot (all in bounds; their values are not used)
+  const size_t ic = slot ? i : row;
   const int s = io.bstart[b], e_end = io.bend[b];
-  const bool m = slot && io.mask[i] != 0;
+  const uint8_t mb = io.mask[ic];
   WavePartial p[PS > 0 ? PS : 1];
   float c = 0.0f, ef = 1.0f, h = 0.0f;
   int tok = -1;
   if constexpr (PS > 0) {
-    if (m) {
 #pragma unroll
-      for (int q = 0; q < PS; ++q) p[q] = parts[i * PS + q];
-    }
+    for (int q = 0; q < PS; ++q) p[q] = parts[ic * PS + q];
   } else {
-    if (m) {
-      c = io.conf[i];
-      if (io.eps) ef = io.eps[i];
-      if (io.x) tok = io.tokens[i];
-    }
+    // absent arrays are stood in for by conf (same extent), read and unused
+    c = io.conf[ic];
+    const float ev = (io.eps ? io.eps : io.conf)[ic];
+    const int32_t tv = (io.x ? io.tokens : reinterpret_cast<const int32_t*>(io.conf))[ic];
+    ef = io.eps ? ev : 1.0f;
+    tok = io.x ? tv : -1;
   }
-  if constexpr (Robust) h = (m && io.eta.eta) ? io.eta.eta[i] : io.eta.uniform;
+  if constexpr (Robust) {
+    // without per-position eta, a float of conf or of the partials stands in
+    const float* stand_in;
+    if constexpr (PS > 0)
+      stand_in = reinterpret_cast<const float*>(parts);
+    else
+      stand_in = io.conf;
+    const float hv = (io.eta.eta ? io.eta.eta : stand_in)[ic];
+    h = io.eta.eta ? hv : io.eta.uniform;
+  }
+  // all of them issue before anything waits for one: a compiler memory fence
+  // keeps the loads above it, a scheduling fence keeps the arithmetic below
+  // (neither emits an instruction; each load's wait comes at its first use)
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_sched_barrier(0);
+  const bool m = slot && mb != 0;
   const bool ok = window_ok(s, e_end, L);
   const bool inwin = ok && lane >= s && lane < e_end;
   const bool valid = inwin && m;
   double e = 1.0;
   if constexpr (PS > 0) {
-    if (valid) {
-      const RowResult rr = combine_parts_regs<PS>(p);
-      store_row(out, i, rr);
-      c = rr.conf;
-      e = (double)rr.eps;
-      tok = rr.token;
-    }
-  } else if (valid) {
-    e = io.eps ? (double)ef : 1.0 - (double)c;   // 1 - c is exact in double
+    const RowResult rr = combine_parts_regs<PS>(p);
+    if (valid) store_row(out, i, rr);
+    c = valid ? rr.conf : 0.0f;
+    e = valid ? (double)rr.eps : 1.0;
+    tok = rr.token;
+  } else {
+    const double ev = io.eps ? (double)ef : 1.0 - (double)c;   // 1 - c is exact in double
+    e = valid ? ev : 1.0;
+    c = valid ? c : 0.0f;
   }
   if constexpr (Robust) e = valid ? fmin(1.0, e + fmax((double)h, 0.0)) : e;
   bool take = false;
