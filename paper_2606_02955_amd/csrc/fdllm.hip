@@ -423,12 +423,15 @@ k_confidence(const typename Vec::Raw* __restrict__ logits, int B, int L, int nve
   const int rloc = wave / S;
   const int w = wave % S;
   const int W = L < kRowGroups ? L : kRowGroups;
-  const long long vs = (long long)blockIdx.x * Shape::kRows + rloc;
-  const bool live = vs < (long long)B * W;
+  // row group index: a launch holds fewer than 2^32 work-items, so fewer
+  // than 2^26 workgroups of at least 64 threads and two row groups at most
+  // each: 32-bit division
+  const unsigned vs = blockIdx.x * (unsigned)Shape::kRows + (unsigned)rloc;
+  const bool live = (unsigned long long)vs < (unsigned long long)B * (unsigned long long)W;
   int b = 0, q = 0, s = 0, len = 0;
   if (live) {
-    b = (int)(vs / W);
-    q = (int)(vs % W);
+    b = (int)(vs / (unsigned)W);
+    q = (int)(vs % (unsigned)W);
     const int s0 = bstart[b], e0 = bend[b];
     if (window_ok(s0, e0, L)) {
       s = s0;
@@ -436,8 +439,9 @@ k_confidence(const typename Vec::Raw* __restrict__ logits, int B, int L, int nve
     }
   }
   const size_t row0 = (size_t)b * L;
-  if (live && w == 0 && lane == 0)
-    for (int j = q; j < L; j += W)
+  // defaults of this row group's positions outside the window, one per lane
+  if (live && w == 0)
+    for (int j = q + lane * W; j < L; j += W * kWave)
       if (j < s || j >= s + len) store_default(out, row0 + j);
   // trips over the window; where row groups of one workgroup meet barriers
   // (S = 2: two row groups), a count that depends on L only
