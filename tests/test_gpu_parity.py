@@ -372,7 +372,12 @@ def test_decode_step_row_parts_match_single_workgroup(gpu, B, L, V, dt, window):
 
 @pytest.mark.parametrize("B,L,V,dt,window", [(260, 32, 126464, torch.bfloat16, 32),
                                               (300, 12, 20000, torch.float32, 12),
-                                              (257, 70, 3000, torch.bfloat16, 70)])
+                                              (257, 70, 3000, torch.bfloat16, 70),
+                                              # the remainder's limits on a 256-CU part: 64 beyond
+                                              # one and two CU multiples, then 65 (all fused)
+                                              (320, 8, 4096, torch.bfloat16, 8),
+                                              (576, 8, 2048, torch.float32, 8),
+                                              (321, 8, 4096, torch.float32, 8)])
 def test_fused_step_remainder_bits(gpu, B, L, V, dt, window):
     """Sequences beyond a multiple of the CU count take the small-batch plan
     beside the fused kernel: the decode step gives fdllm_confidence's bits for
