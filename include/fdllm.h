@@ -230,10 +230,13 @@ fdllm_status fdllm_decode_step(const void* logits, fdllm_dtype dtype, int B, int
  * the library runs on, held until the process ends.  The call allocates and
  * frees nothing.
  *   Sizes whose workspace exceeds FDLLM_STATIC_SCRATCH_BYTES are refused with
- *   FDLLM_ERR_SCRATCH (nothing enqueued).  Batches of 256 sequences or more
- *   need no scratch at all; smaller ones need 12 B per position of the span
- *   (when tokens, conf or eps are not given) plus up to 384 B per position of
- *   blocks of at most 64 positions.
+ *   FDLLM_ERR_SCRATCH (nothing enqueued).  Small batches need 12 B per
+ *   position of the span (when tokens, conf or eps are not given) plus up to
+ *   384 B per position of blocks of at most 64 positions; batches of 256
+ *   sequences or more need scratch only for the at most 64 sequences beyond a
+ *   multiple of the compute-unit count, which run as a small batch.  Those
+ *   run on `stream` after the one-kernel part instead of beside it on a side
+ *   stream (the call creates no stream and no event), with the same bits.
  *   Every call on one GPU uses that GPU's one array: calls that overlap on one
  *   GPU (other streams, other threads) race and must be serialised by the
  *   caller.  The array keeps the last call's contents; the step needs none of

@@ -20,6 +20,7 @@
 #include <mutex>
 
 #include "fdllm.h"
+#include "pass_common.h"
 
 namespace {
 
@@ -72,6 +73,9 @@ extern "C" fdllm_status fdllm_decode_step_static(
     ws = scratch_on_current_device(&st);
     if (!ws) return st;
   }
-  return fdllm_decode_step(logits, dtype, B, L, V, mask, block_start, block_end, x, sel, param, eta,
-                           eta_uniform, tokens, conf, eps, lse, commit, n_commit, ws, need, stream);
+  // a large batch's last sequences run after its one-kernel part on `stream`
+  // (no side stream, no events), with the same bits
+  return fdllm::decode_step(logits, dtype, B, L, V, mask, block_start, block_end, x, sel, param, eta,
+                            eta_uniform, tokens, conf, eps, lse, commit, n_commit, ws, need, stream,
+                            false);
 }

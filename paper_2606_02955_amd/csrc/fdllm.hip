@@ -1604,6 +1604,21 @@ fdllm_status fdllm_decode_step(const void* logits, fdllm_dtype dtype, int B, int
                                float eta_uniform, int32_t* tokens, float* conf, float* eps,
                                float* lse, uint8_t* commit, int32_t* n_commit, void* workspace,
                                size_t workspace_bytes, fdllm_stream stream) {
+  return fdllm::decode_step(logits, dtype, B, L, V, mask, block_start, block_end, x, sel, param, eta,
+                            eta_uniform, tokens, conf, eps, lse, commit, n_commit, workspace,
+                            workspace_bytes, stream, true);
+}
+
+}  // extern "C"
+
+namespace fdllm {
+
+fdllm_status decode_step(const void* logits, fdllm_dtype dtype, int B, int L, int V, uint8_t* mask,
+                         const int32_t* block_start, const int32_t* block_end, int32_t* x,
+                         fdllm_selector sel, float param, const float* eta, float eta_uniform,
+                         int32_t* tokens, float* conf, float* eps, float* lse, uint8_t* commit,
+                         int32_t* n_commit, void* workspace, size_t workspace_bytes,
+                         fdllm_stream stream, bool side_stream_ok) {
   if (dtype != FDLLM_BF16 && dtype != FDLLM_F32) return FDLLM_ERR_UNSUPPORTED_DTYPE;
   if (sel != FDLLM_SEL_THRESHOLD && sel != FDLLM_SEL_FACTOR && sel != FDLLM_SEL_PROFILE &&
       sel != FDLLM_SEL_ROBUST)
@@ -1623,24 +1638,36 @@ fdllm_status fdllm_decode_step(const void* logits, fdllm_dtype dtype, int B, int
   const int b0 = B - p.rem;
   const Plan q = remainder_plan(p);
   const bool outs_given = tokens && conf && eps;
+  const bool rem_ok = p.rem && (outs_given || (workspace && workspace_bytes >= workspace_bytes_for(B, L, p)));
+  const size_t r0 = (size_t)b0 * (size_t)L;
+  const size_t esize = dtype == FDLLM_BF16 ? 2 : 4;
+  auto off = [](auto* ptr, size_t k) { return ptr ? ptr + k : ptr; };
+  // sequences [b0, B) as a small batch (the same launches on either stream)
+  auto remainder = [&](hipStream_t on) {
+    return step_split(q, sel, (const char*)logits + r0 * (size_t)V * esize, dtype, p.rem, L, V,
+                      mask + r0, block_start + b0, block_end + b0, x + r0, param,
+                      EtaIn{off(eta, r0), eta_uniform}, off(tokens, r0), off(conf, r0),
+                      off(eps, r0), off(lse, r0), off(commit, r0), off(n_commit, (size_t)b0),
+                      workspace, workspace_bytes, on);
+  };
+  if (rem_ok && !side_stream_ok) {
+    // no side stream and no events: the remainder after the fused kernel, on
+    // the caller's stream (the same kernels and bits, without the overlap)
+    if (launch_fused(sel, logits, dtype, b0, L, V, mask, block_start, block_end, x, param, etain, out,
+                     commit, n_commit, st) != hipSuccess)
+      return FDLLM_ERR_HIP;
+    return remainder(st);
+  }
   hipStream_t side = nullptr;
-  if (p.rem && (outs_given || (workspace && workspace_bytes >= workspace_bytes_for(B, L, p))) &&
-      side_stream(&side) == hipSuccess) {
+  if (rem_ok && side_stream(&side) == hipSuccess) {
     // sequences [b0, B) on the side stream, forked from and joined back to
     // the caller's stream by events, at the same time as the fused kernel
-    const size_t r0 = (size_t)b0 * (size_t)L;
-    const size_t esize = dtype == FDLLM_BF16 ? 2 : 4;
-    auto off = [](auto* ptr, size_t k) { return ptr ? ptr + k : ptr; };
     hipEvent_t fork = nullptr, join = nullptr;
     fdllm_status res = FDLLM_ERR_HIP;
     if (hipEventCreateWithFlags(&fork, hipEventDisableTiming) == hipSuccess &&
         hipEventCreateWithFlags(&join, hipEventDisableTiming) == hipSuccess &&
         hipEventRecord(fork, st) == hipSuccess && hipStreamWaitEvent(side, fork, 0) == hipSuccess) {
-      res = step_split(q, sel, (const char*)logits + r0 * (size_t)V * esize, dtype, p.rem, L, V,
-                       mask + r0, block_start + b0, block_end + b0, x + r0, param,
-                       EtaIn{off(eta, r0), eta_uniform}, off(tokens, r0), off(conf, r0),
-                       off(eps, r0), off(lse, r0), off(commit, r0), off(n_commit, (size_t)b0),
-                       workspace, workspace_bytes, side);
+      res = remainder(side);
       if (res == FDLLM_OK && hipEventRecord(join, side) != hipSuccess) res = FDLLM_ERR_HIP;
       if (res == FDLLM_OK &&
           launch_fused(sel, logits, dtype, b0, L, V, mask, block_start, block_end, x, param, etain,
@@ -1658,4 +1685,4 @@ fdllm_status fdllm_decode_step(const void* logits, fdllm_dtype dtype, int B, int
   return err == hipSuccess ? FDLLM_OK : FDLLM_ERR_HIP;
 }
 
-}  // extern "C"
+}  // namespace fdllm

@@ -273,6 +273,18 @@ hipError_t launch_select(fdllm_selector sel, const SelectIO& io, int B, int L, f
 
 inline size_t align256(size_t n) { return (n + 255) & ~(size_t)255; }
 
+// Host side, defined with the decode-step kernels: fdllm_decode_step, whose
+// large batches may run their last sequences on a side stream beside the
+// one-kernel part.  Without side_stream_ok those sequences run after it on
+// `stream` instead (same kernels, same bits), so the call creates no stream
+// and no event (fdllm_decode_step_static).
+fdllm_status decode_step(const void* logits, fdllm_dtype dtype, int B, int L, int V, uint8_t* mask,
+                         const int32_t* block_start, const int32_t* block_end, int32_t* x,
+                         fdllm_selector sel, float param, const float* eta, float eta_uniform,
+                         int32_t* tokens, float* conf, float* eps, float* lse, uint8_t* commit,
+                         int32_t* n_commit, void* workspace, size_t workspace_bytes,
+                         fdllm_stream stream, bool side_stream_ok);
+
 }  // namespace fdllm
 
 #endif  // FDLLM_PASS_COMMON_H

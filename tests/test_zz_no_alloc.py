@@ -63,13 +63,16 @@ def _same(a, b):
 
 # shrinking inputs: every plan that uses scratch (rows split over several
 # workgroups with their parts in scratch; rows split within a workgroup; wide
-# spans), one that needs none (256 sequences: one workgroup per sequence), and
+# spans), large batches (one workgroup per sequence, their last sequences
+# beyond a multiple of the CU count as a small batch: on a side stream for
+# fdllm_decode_step, after the one-kernel part for the static call), and
 # calls without tokens / conf / eps, whose values then live in the scratch
 CASES = [
     (8, 32, 126464, torch.bfloat16, "profile", 1.0, True),
     (2, 16, 126464, torch.bfloat16, "factor", 1.0, False),
     (40, 64, 50000, torch.bfloat16, "threshold", 0.9, True),
     (3, 32, 5000, torch.float32, "robust", 0.9, False),
+    (300, 8, 4096, torch.float32, "threshold", 0.9, False),
     (260, 8, 4096, torch.bfloat16, "profile", 0.75, True),
     (24, 200, 8000, torch.bfloat16, "profile", 1.0, False),
     (1, 32, 126464, torch.float32, "profile", 1.0, False),
