@@ -193,8 +193,8 @@ fdllm_status fdllm_reveal(const uint8_t* commit, const int32_t* tokens, int32_t*
  * batch exceeds a multiple of the GPU's compute-unit count by at most 64
  * sequences, those last sequences run with the small-batch kernels on a
  * stream the library keeps per device, at the same time as the one-kernel
- * part; the call stays asynchronous (the side stream is forked from and
- * joined back to `stream` by events).  That needs the workspace, or tokens,
+ * part; the call stays asynchronous and can be captured into a HIP graph
+ * (the side stream is forked from and joined back to `stream` by events).  That needs the workspace, or tokens,
  * conf and eps all given; without either, they run in the one kernel.
  *   eta, eta_uniform: calibration allowance of FDLLM_SEL_ROBUST (as in
  *   fdllm_select_robust); ignored by the other selectors.
