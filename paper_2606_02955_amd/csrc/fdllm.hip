@@ -70,8 +70,8 @@
 #ifndef FDLLM_FUSED_MIN_B
 #define FDLLM_FUSED_MIN_B 256     // batches from this size run one workgroup per sequence
 #endif
-#ifndef FDLLM_ROW_GROUPS
-#define FDLLM_ROW_GROUPS 64       // small batches: window-relative row groups per sequence (at most)
+#ifndef FDLLM_GROUPS32_MIN_B
+#define FDLLM_GROUPS32_MIN_B 8    // small batches from this size: 32 row groups per sequence, not 64
 #endif
 #ifndef FDLLM_HYBRID_MAX_REM
 #define FDLLM_HYBRID_MAX_REM 64   // sequences beyond a multiple of the CU count run on a side stream
@@ -81,8 +81,17 @@
 #endif
 
 namespace fdllm {
-constexpr int kRowGroups = FDLLM_ROW_GROUPS;   // row groups per sequence of the split pass (at most)
-static_assert(kRowGroups >= 1 && kRowGroups <= 64, "row groups");
+// Row groups per sequence of the split pass (window positions q, q + W, ...
+// of a row group): 64, one wavefront's block, for the fewest sequences,
+// where a wider window's rows should all stream at once; 32, the paper's
+// block, from FDLLM_GROUPS32_MIN_B sequences, where the grid is half as
+// large and a 64-wide window's second row per group still finds the chip
+// busy; never more than the span.
+constexpr int kGroups32MinB = FDLLM_GROUPS32_MIN_B;
+__host__ __device__ inline int row_groups(int B, int L) {
+  const int g = B >= kGroups32MinB ? 32 : 64;
+  return L < g ? L : g;
+}
 
 // ---------------------------------------------------------------------------
 // vector formats: one lane loads 16 bytes (or one element on the scalar path)
@@ -406,7 +415,7 @@ __device__ __forceinline__ RowResult combine_parts(const WavePartial* part) {
 }
 
 // Row group r of the grid handles the window-relative slot (b, q), q < W =
-// min(L, 64): the window positions q, q + W, ... of sequence b (one for a
+// row_groups(B, L): the window positions q, q + W, ... of sequence b (one for a
 // window of at most W positions), and the defaults of the positions j = q,
 // q + W, ... of the whole row of L slots that lie outside the window.  So
 // only B W row groups are launched, however long the span L.
@@ -422,7 +431,7 @@ k_confidence(const typename Vec::Raw* __restrict__ logits, int B, int L, int nve
   const int lane = threadIdx.x % kWave;
   const int rloc = wave / S;
   const int w = wave % S;
-  const int W = L < kRowGroups ? L : kRowGroups;
+  const int W = row_groups(B, L);
   // row group index: a launch holds fewer than 2^32 work-items, so fewer
   // than 2^26 workgroups of at least 64 threads and two row groups at most
   // each: 32-bit division
@@ -1155,7 +1164,7 @@ constexpr int kTargetWaves = FDLLM_TARGET_WAVES;   // row-streaming waves the sp
 
 static Plan make_plan(int B, int L, int V, fdllm_dtype dt) {
   Plan p{};
-  const long long win = L < kRowGroups ? L : kRowGroups;
+  const long long win = row_groups(B, L);
   p.fused = B >= kFusedMinB;
   p.split = 1;
   if (p.fused) {
@@ -1193,7 +1202,7 @@ template <class Vec>
 static hipError_t launch_confidence_t(const void* logits, int B, int L, int nvec, int split,
                                       const uint8_t* mask, const int32_t* bs, const int32_t* be,
                                       RowOut out, hipStream_t st) {
-  const long long nvslots = (long long)B * (L < kRowGroups ? L : kRowGroups);   // window-relative
+  const long long nvslots = (long long)B * row_groups(B, L);   // window-relative
   const auto* lg = (const typename Vec::Raw*)logits;
 #define FDLLM_CONF_CASE(SPLIT)                                                                  \
   case SPLIT: {                                                                                 \
