@@ -52,6 +52,9 @@ SMALL = [
     (257, 3, 7, torch.bfloat16, None),        # fused plan, scalar path
     (2, 24, 40000, torch.bfloat16, 24),       # rows split 8 ways (decode: two workgroups per row)
     (1, 20, 70001, torch.bfloat16, None),     # split 16 ways, scalar path
+    (8, 64, 6000, torch.float32, 64),         # from 8 sequences: 32 row groups, two rows each
+    (7, 48, 3000, torch.bfloat16, None),      # below 8 sequences: 64 row groups
+    (16, 40, 20000, torch.bfloat16, 40),      # 32 row groups, windows of 33-40 rows
 ]
 
 # blocks beyond one wavefront (block-size ablation): workgroup selection
