@@ -1164,7 +1164,10 @@ constexpr int kTargetWaves = FDLLM_TARGET_WAVES;   // row-streaming waves the sp
 
 static Plan make_plan(int B, int L, int V, fdllm_dtype dt) {
   Plan p{};
-  const long long win = row_groups(B, L);
+  // slots per sequence the split aims to fill: spans of at most one
+  // wavefront count every position (the parts kernel has a slot for each),
+  // longer spans their window-relative row groups
+  const long long win = L <= kWaveBlock ? L : row_groups(B, L);
   p.fused = B >= kFusedMinB;
   p.split = 1;
   if (p.fused) {
