@@ -1,8 +1,9 @@
 """The decode step captured into a HIP graph (torch.cuda.CUDAGraph) and
 replayed: a large batch whose last sequences run on the library's side stream
 (forked from and joined back to the capturing stream by events), the same
-with those sequences' conf and eps in the workspace, a small batch (two
-launches), and the static-scratch entry point.  Every replay, with eager work
+with those sequences' conf and eps in the workspace, small batches (two
+launches; one of them with windows wider than a wavefront), and the
+static-scratch entry point.  Every replay, with eager work
 between replays, must give the eager call's outputs bit for bit."""
 import pytest
 import torch
@@ -27,6 +28,7 @@ def _outs(B, L, dev, scores):
     (260, 8, 4096, torch.bfloat16, True, False),    # 4 sequences beyond 256 CUs, outputs given
     (300, 8, 2048, torch.float32, False, False),    # 44 beyond, their conf / eps in the workspace
     (8, 32, 20000, torch.bfloat16, False, False),   # a small batch: the pass, then the selection
+    (16, 300, 3000, torch.bfloat16, True, False),   # 32 row groups over 300-wide windows, wide selection
     (300, 8, 2048, torch.float32, False, True),     # the static entry point: no side stream
     (8, 32, 20000, torch.bfloat16, False, True),
 ])
